@@ -1,0 +1,289 @@
+"""Proximity-graph construction for the synthetic workloads.
+
+The search method takes the graph as a given input (the paper builds it
+offline with Vamana plus JAG threshold pruning, Sec. II "Graph
+construction"). This module is that offline step for the synthetic data,
+and it is deliberately not the paper's builder:
+
+  1. exact kNN candidates (2R per point, ordered by distance then id);
+  2. relative-neighbourhood pruning with slack alpha (a candidate v is
+     dropped when an already kept w satisfies alpha * d(w, v) <= d(u, v)),
+     the DiskANN/Vamana diversification rule;
+  3. a flat navigation layer: a seeded sample of points plus one
+     representative per connected component of the pruned kNN graph.
+     Each sample point links to sample points of other components, chosen
+     by the same alpha-pruning (so roughly one per nearby component), and
+     every point links to its nearest sample points. Clustered mixtures
+     otherwise give one disconnected kNN component per cluster;
+  4. connectivity repair: every point is made reachable from the entry
+     point (the point nearest the data centroid).
+
+Rows are fixed-width n x R uint32 with 0xFFFFFFFF padding. Everything is
+deterministic for a given device. Distances here are this module's own
+(float64 on the CPU, float32 GEMM on a GPU) and share no code with either
+search implementation.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+PAD = 0xFFFFFFFF
+
+
+def _as_float(x: np.ndarray, dev: torch.device) -> torch.Tensor:
+    dt = torch.float64 if dev.type == "cpu" else torch.float32
+    return torch.from_numpy(np.ascontiguousarray(x)).to(dev).to(dt)
+
+
+def entry_point(vectors: np.ndarray) -> int:
+    """Id of the point nearest (float64 L2) to the float64 centroid; lowest id on ties."""
+    n = vectors.shape[0]
+    c = np.zeros(vectors.shape[1], dtype=np.float64)
+    step = 1 << 16
+    for s in range(0, n, step):
+        c += vectors[s:s + step].astype(np.float64).sum(axis=0)
+    c /= n
+    best, best_d = -1, np.inf
+    for s in range(0, n, step):
+        x = vectors[s:s + step].astype(np.float64)
+        dd = ((x - c) ** 2).sum(axis=1)
+        j = int(np.argmin(dd))
+        if dd[j] < best_d:
+            best, best_d = s + j, float(dd[j])
+    return best
+
+
+def _sq_dist(a: torch.Tensor, b: torch.Tensor, na: torch.Tensor, nb: torch.Tensor) -> torch.Tensor:
+    d = na[:, None] + nb[None, :] - 2.0 * (a @ b.T)
+    return d.clamp_min_(0)
+
+
+def _sort_by_dist_then_id(dist: torch.Tensor, ids: torch.Tensor):
+    o = torch.argsort(ids, dim=1, stable=True)
+    dist, ids = dist.gather(1, o), ids.gather(1, o)
+    o = torch.argsort(dist, dim=1, stable=True)
+    return dist.gather(1, o), ids.gather(1, o)
+
+
+def knn(X: torch.Tensor, K: int, targets: torch.Tensor | None = None, exclude_self=True,
+        chunk: int = 4096):
+    """K nearest rows of `targets` (default X) for every row of X; (dist, ids) sorted."""
+    T = X if targets is None else targets
+    nx = (X * X).sum(1)
+    nt = nx if targets is None else (T * T).sum(1)
+    n = X.shape[0]
+    out_d = torch.empty((n, K), dtype=X.dtype, device=X.device)
+    out_i = torch.empty((n, K), dtype=torch.int64, device=X.device)
+    extra = 4  # margin so ties at the boundary resolve by id
+    kk = min(K + extra + (1 if exclude_self else 0), T.shape[0])
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        D = _sq_dist(X[s:e], T, nx[s:e], nt)
+        if exclude_self:
+            r = torch.arange(s, e, device=X.device)
+            D[r - s, r] = float("inf")
+        dv, di = torch.topk(D, kk, dim=1, largest=False, sorted=True)
+        dv, di = _sort_by_dist_then_id(dv, di)
+        out_d[s:e], out_i[s:e] = dv[:, :K], di[:, :K]
+        del D
+    return out_d, out_i
+
+
+def alpha_prune(X: torch.Tensor, cand: torch.Tensor, du: torch.Tensor, valid: torch.Tensor,
+                budget: torch.Tensor, alpha: float, chunk: int = 8192) -> torch.Tensor:
+    """Greedy diversification of each row's sorted candidates; returns keep mask."""
+    n, K = cand.shape
+    keep_all = torch.zeros((n, K), dtype=torch.bool, device=X.device)
+    a2 = alpha * alpha
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        c = cand[s:e].clamp_min(0)
+        V = X[c]                                   # B x K x d
+        nv = (V * V).sum(-1)
+        G = torch.bmm(V, V.transpose(1, 2).contiguous())
+        Dvv = (nv[:, :, None] + nv[:, None, :] - 2.0 * G).clamp_min_(0)
+        dus = du[s:e]
+        val = valid[s:e]
+        bud = budget[s:e]
+        keep = torch.zeros((e - s, K), dtype=torch.bool, device=X.device)
+        cnt = torch.zeros(e - s, dtype=torch.int64, device=X.device)
+        for j in range(K):
+            if j > 0:
+                dom = (keep[:, :j] & (a2 * Dvv[:, :j, j] <= dus[:, j:j + 1])).any(1)
+            else:
+                dom = torch.zeros(e - s, dtype=torch.bool, device=X.device)
+            ok = val[:, j] & ~dom & (cnt < bud)
+            keep[:, j] = ok
+            cnt += ok.to(torch.int64)
+        keep_all[s:e] = keep
+        del V, G, Dvv
+    return keep_all
+
+
+def _compact(a: torch.Tensor, width: int) -> torch.Tensor:
+    """Move the non-negative entries of each row to the front (order kept)."""
+    o = torch.argsort((a < 0).to(torch.int8), dim=1, stable=True)
+    return a.gather(1, o)[:, :width]
+
+
+def _components(n: int, rows: np.ndarray) -> np.ndarray:
+    from scipy.sparse import coo_matrix
+    from scipy.sparse.csgraph import connected_components
+    src = np.repeat(np.arange(n, dtype=np.int64), rows.shape[1])
+    dst = rows.reshape(-1).astype(np.int64)
+    ok = dst >= 0
+    g = coo_matrix((np.ones(int(ok.sum()), dtype=np.int8), (src[ok], dst[ok])), shape=(n, n)).tocsr()
+    _, lab = connected_components(g, directed=False)
+    return lab
+
+
+def _reachable(n: int, adj: np.ndarray, s: int) -> np.ndarray:
+    from scipy.sparse import csr_matrix
+    from scipy.sparse.csgraph import breadth_first_order
+    R = adj.shape[1]
+    a = adj.astype(np.int64)
+    a[adj == PAD] = -1
+    ok = a >= 0
+    indptr = np.zeros(n + 1, dtype=np.int64)
+    indptr[1:] = np.cumsum(ok.sum(1))
+    g = csr_matrix((np.ones(int(ok.sum()), dtype=np.int8), a[ok], indptr), shape=(n, n))
+    order = breadth_first_order(g, s, directed=True, return_predecessors=False)
+    seen = np.zeros(n, dtype=bool)
+    seen[order] = True
+    return seen
+
+
+def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
+                alpha: float = 1.2, seed: int = 0x9A9A, entry: int | None = None):
+    """Fixed-degree proximity graph; returns (adjacency n x R uint32, entry id)."""
+    dev = torch.device(device)
+    n = vectors.shape[0]
+    s_id = entry_point(vectors) if entry is None else int(entry)
+    X = _as_float(vectors, dev)
+    Kc = min(2 * R, n - 1)
+
+    # 1-2: exact kNN candidates, pruned.
+    du, cand = knn(X, Kc)
+    R_long = max(1, R // 16)
+    K_nav = max(2, R // 2)
+
+    # 3: navigation sample (seeded sample + component representatives + entry).
+    base_budget = torch.full((n,), R - R_long, dtype=torch.int64, device=dev)
+    keep0 = alpha_prune(X, cand, du, torch.ones_like(cand, dtype=torch.bool), base_budget, alpha)
+    rows0 = torch.where(keep0, cand, torch.full_like(cand, -1)).cpu().numpy()
+    lab = _components(n, rows0)
+    first_of = np.full(lab.max() + 1, n, dtype=np.int64)
+    np.minimum.at(first_of, lab, np.arange(n))
+    g = np.random.Generator(np.random.PCG64(seed))
+    m0 = min(n, int(math.ceil(2 * math.sqrt(n))))
+    P = np.unique(np.concatenate([first_of, g.choice(n, size=m0, replace=False), [s_id]]))
+    Pt = torch.from_numpy(P).to(dev)
+    XP = X[Pt]
+    is_nav = torch.zeros(n, dtype=torch.bool, device=dev)
+    is_nav[Pt] = True
+
+    # sample-to-sample links: alpha-pruning over each sample's nearest
+    # samples in OTHER components (the kNN graph already connects a
+    # component internally), so each sample links to nearby components.
+    KP = min(len(P) - 1, 256)
+    dPP, iPP = knn(XP, KP)
+    labP = torch.from_numpy(lab[P]).to(dev)
+    other = labP[iPP] != labP[:, None]
+    nav_keep = alpha_prune(XP, iPP, dPP, other,
+                           torch.full((len(P),), K_nav, dtype=torch.int64, device=dev), alpha)
+    nav_ids = _compact(torch.where(nav_keep, Pt[iPP], torch.full_like(iPP, -1)), K_nav)
+    nav_links = torch.full((n, K_nav), -1, dtype=torch.int64, device=dev)
+    nav_links[Pt] = nav_ids
+
+    # every point: its nearest sample points other than itself.
+    _, iNear = knn(X, R_long + 1, targets=XP, exclude_self=False)
+    near = Pt[iNear]
+    near = _compact(torch.where(near == torch.arange(n, device=dev)[:, None],
+                                torch.full_like(near, -1), near), R_long)
+
+    long = torch.cat([nav_links, near], 1)
+    dup = torch.zeros_like(long, dtype=torch.bool)
+    for j in range(1, long.shape[1]):
+        dup[:, j] = (long[:, :j] == long[:, j:j + 1]).any(1)
+    long = _compact(torch.where(dup, torch.full_like(long, -1), long), long.shape[1])
+    n_long = (long >= 0).sum(1)
+
+    # base candidates not already linked, pruned into the remaining budget.
+    in_long = torch.zeros_like(cand, dtype=torch.bool)
+    for j in range(long.shape[1]):
+        in_long |= cand == long[:, j:j + 1]
+    keep = alpha_prune(X, cand, du, ~in_long, R - n_long, alpha)
+
+    adj = np.full((n, R), PAD, dtype=np.uint32)
+    longn = long.cpu().numpy()
+    candn = cand.cpu().numpy()
+    keepn = keep.cpu().numpy()
+    for_rows = np.full((n, R), -1, dtype=np.int64)
+    # compact: long links first, then kept base candidates in distance order
+    merged = np.concatenate([longn, np.where(keepn, candn, -1)], axis=1)
+    order = np.argsort(merged < 0, axis=1, kind="stable")
+    merged = np.take_along_axis(merged, order, axis=1)[:, :R]
+    for_rows[:, :merged.shape[1]] = merged
+    adj[for_rows >= 0] = for_rows[for_rows >= 0].astype(np.uint32)
+
+    # 4: connectivity repair from the entry point.
+    print('unreachable before repair', int((~_reachable(n, adj, s_id)).sum()))
+    adj = repair(adj, vectors, s_id, P, cand.cpu().numpy())
+    return adj, s_id
+
+
+def repair(adj: np.ndarray, vectors: np.ndarray, s_id: int, P: np.ndarray,
+           cand: np.ndarray, rounds: int = 8):
+    """Make every point reachable from s_id.
+
+    An unreachable point v gets an in-edge from the nearest reachable point
+    among its own kNN candidates (else the nearest reachable sample point):
+    into a padding slot if the row has one, else replacing the row's
+    farthest out-edge whose target keeps another in-edge.
+    """
+    n, R = adj.shape
+    indeg = np.bincount(adj[adj != PAD].astype(np.int64), minlength=n)
+    for _ in range(rounds):
+        seen = _reachable(n, adj, s_id)
+        if seen.all():
+            return adj
+        ok_P = P[seen[P]]
+        ok_Pf = vectors[ok_P].astype(np.float64)
+        for v in np.flatnonzero(~seen):
+            if seen[v]:
+                continue
+            ws = [int(w) for w in cand[v] if w >= 0 and seen[w]]
+            if not ws:
+                x = vectors[v].astype(np.float64)
+                ws = [int(ok_P[i]) for i in np.argsort(((ok_Pf - x) ** 2).sum(1), kind="stable")[:64]]
+            for w in ws:
+                if w == v:
+                    continue
+                row = adj[w]
+                pads = np.flatnonzero(row == PAD)
+                if pads.size:
+                    slot = int(pads[0])
+                else:
+                    movable = [j for j in range(R - 1, -1, -1) if indeg[row[j]] >= 2]
+                    if not movable:
+                        continue
+                    slot = movable[0]
+                    indeg[row[slot]] -= 1
+                row[slot] = v
+                indeg[v] += 1
+                break
+            stack = [v]
+            seen[v] = True
+            while stack:
+                u = stack.pop()
+                for t in adj[u]:
+                    if t != PAD and not seen[t]:
+                        seen[t] = True
+                        stack.append(int(t))
+    seen = _reachable(n, adj, s_id)
+    if not seen.all():
+        raise RuntimeError(f"graph repair left {int((~seen).sum())} unreachable points")
+    return adj
