@@ -1,0 +1,163 @@
+/*
+ * boa.h — C ABI of the MI355X (gfx950) filtered beam search with online
+ * beamwidth adaptation ("BOA: Beamwidth Online Adaptation for
+ * Filtered-ANNS on a GPU").
+ *
+ * Problem (Sec. II, Def. 1 and Def. 2): each base point carries a vector
+ * and m numeric attributes; a query carries a vector and one inclusive
+ * range [lo, hi] per attribute (Eq. 2). The answer is the k points nearest
+ * to the query vector (Euclidean) among those satisfying every range.
+ *
+ * Method: every query is searched first at a narrow beamwidth L0; queries
+ * whose result fails the confidence test (Eq. 3) are compacted on the
+ * device and searched again, from scratch, at the next wider width
+ * (Alg. 1); each search is the filter-aware beam search of Alg. 2 with
+ * exact squared-L2 distances. BOA+ (Sec. III-A "Pipelining Multiple
+ * Batches") issues the first phase as sub-batches on one stream while the
+ * pooled survivors are escalated on a second stream.
+ *
+ * Conventions for every entry point:
+ *   - Return value: BOA_OK (0) or a negative BOA_E* code; no C++ exception
+ *     crosses this boundary and the library never aborts. On a non-zero
+ *     return, boa_last_error() describes the failure (thread-local string).
+ *   - Validation happens before any device work: on BOA_EINVAL the output
+ *     buffers are untouched.
+ *   - Attribute and range cells are 4 bytes: int32 for BOA_ATTR_I32
+ *     columns, the IEEE bit pattern of a float32 for BOA_ATTR_F32 columns.
+ *   - Distances are squared Euclidean distances in float32 (exact integers
+ *     for uint8 data). float32 distances use one fixed summation order:
+ *     16 partial sums, chunk c = dims 4c..4c+3 accumulated into partial
+ *     c mod 16 by fused multiply-add of the float32 difference, chunks in
+ *     increasing order, then the partials summed pairwise (p += p+8, +4,
+ *     +2, +1).
+ *   - Search ordering is lexicographic on (number of violated predicates,
+ *     distance, id): the filter penalty of Alg. 2 taken larger than any
+ *     distance, ties broken by id.
+ *   - Not thread-safe per index: one boa_search at a time per boa_index.
+ */
+#ifndef BOA_H
+#define BOA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct boa_index boa_index; /* opaque; owns all of its device memory */
+
+enum {
+    BOA_OK = 0,
+    BOA_EINVAL = -1,       /* invalid argument */
+    BOA_ENOMEM = -2,       /* host or device allocation failed */
+    BOA_EHIP = -3,         /* HIP runtime error */
+    BOA_EUNSUPPORTED = -4, /* valid but not supported by this build */
+    BOA_EOVERFLOW = -5     /* a per-query visited table overflowed (results invalid) */
+};
+
+enum { BOA_VEC_F32 = 0, BOA_VEC_U8 = 1 };
+enum { BOA_ATTR_I32 = 0, BOA_ATTR_F32 = 1 };
+
+#define BOA_MAX_M 8          /* attributes per point */
+#define BOA_MAX_R 64         /* graph out-degree */
+#define BOA_MAX_L 2048       /* beamwidth */
+#define BOA_MAX_PHASES 32
+#define BOA_MAX_N ((int64_t)1 << 24) /* ids are packed into 24 bits */
+
+/*
+ * Build an index from host arrays (copied into device memory; the caller
+ * may free its arrays on return).
+ *   vectors     host, row-major n x d; float32 (BOA_VEC_F32) or uint8 (BOA_VEC_U8).
+ *               d % 4 == 0 (float32) or d % 16 == 0 (uint8); d <= 1024.
+ *   attrs       host, row-major n x m 4-byte cells; 1 <= m <= BOA_MAX_M.
+ *   attr_dtypes host, m entries of BOA_ATTR_I32 / BOA_ATTR_F32.
+ *   adjacency   host, row-major n x R uint32 neighbour ids, padded with
+ *               0xFFFFFFFF; 1 <= R <= BOA_MAX_R. A row may not hold its own
+ *               id. (Graph construction is an offline step: Sec. II.)
+ *   entry       the entry point s of every search (Alg. 2), 0 <= entry < n.
+ *   n           1 <= n < BOA_MAX_N.
+ *   out         receives the index; free it with boa_free_index.
+ * Errors: BOA_EINVAL (bad sizes, null pointers, out-of-range ids in the
+ * adjacency), BOA_ENOMEM, BOA_EHIP.
+ */
+int boa_build_index_from_arrays(const void *vectors, int64_t n, int32_t d, int32_t vec_dtype,
+                                const int32_t *attrs, int32_t m, const int32_t *attr_dtypes,
+                                const uint32_t *adjacency, int32_t R, int64_t entry,
+                                boa_index **out);
+
+/* Search parameters (Alg. 1 inputs). boa_default_params fills the defaults. */
+typedef struct {
+    int32_t k;              /* neighbours returned; 1 <= k <= L of the first phase */
+    int32_t L0;             /* first-phase beamwidth (L_min of Alg. 1) */
+    int32_t Lmax;           /* widest beamwidth; the phase at Lmax is the last */
+    double alpha;           /* growth factor > 1: L <- min(ceil(alpha * L), Lmax); default 2 */
+    double eps;             /* confidence threshold of Eq. 3; default 0.05 */
+    double tau;             /* residual fraction: a phase runs while more than tau*nq
+                               queries are active; 0 <= tau < 1; default 0 */
+    int32_t fixed_L;        /* > 0: a single non-adaptive phase at this width (the
+                               fixed-beamwidth baseline); overrides L0/Lmax/schedule */
+    int32_t boa_plus;       /* 1: BOA+ sub-batched first phase overlapped with escalation */
+    int32_t sub_batches;    /* BOA+ first-phase sub-batches; default 10 */
+    int32_t lds_hash_slots; /* 0: automatic; else a power of two >= 64 that forces the
+                               per-wave LDS visited-table size (tests force spills) */
+    const int32_t *schedule; /* optional host array of explicit phase widths
+                                (strictly increasing); overrides L0/Lmax/alpha */
+    int32_t n_schedule;
+} boa_params;
+
+void boa_default_params(boa_params *p);
+
+/*
+ * Batched adaptive filtered search.
+ *   queries   DEVICE, nq x d, same element type as the index vectors.
+ *   ranges    DEVICE, nq x m x 2 cells [lo, hi] (inclusive), per-column type;
+ *             an unconstrained attribute is [INT32_MIN, INT32_MAX] or [-inf, +inf].
+ *   nq        >= 0 (0 is a no-op).
+ *   ids       DEVICE, nq x k uint32: ids of the valid points found, nearest first;
+ *             0xFFFFFFFF where fewer than k valid points were found.
+ *   dists     DEVICE, nq x k float32 squared distances (+inf in padded slots).
+ *   final_L   DEVICE, nq int32: beamwidth of the phase that produced the result.
+ *   expansions, scored  DEVICE nq uint32 each, or NULL: per query, nodes expanded
+ *             and nodes scored, summed over the phases the query ran in.
+ *   stream    hipStream_t of the caller (NULL = default stream). Device buffers
+ *             must be valid on it. The call returns after the results are
+ *             complete (it synchronises the stream once at the end).
+ * Errors: BOA_EINVAL, BOA_EUNSUPPORTED, BOA_ENOMEM, BOA_EHIP, BOA_EOVERFLOW.
+ */
+int boa_search(boa_index *idx, const void *queries, const int32_t *ranges, int64_t nq,
+               const boa_params *p, uint32_t *ids, float *dists, int32_t *final_L,
+               uint32_t *expansions, uint32_t *scored, void *stream);
+
+/* Statistics of the last boa_search on this index, one row per phase. */
+typedef struct {
+    int32_t L;              /* phase beamwidth */
+    int32_t active;         /* queries searched in the phase */
+    int32_t confident;      /* of which resolved by the confidence test */
+    int32_t launches;       /* kernel launches of the phase (BOA+: sub-batches) */
+    int64_t expansions;     /* nodes expanded, summed over the phase's queries */
+    int64_t scored;         /* nodes scored (distance + predicates) */
+    double gathered_bytes;  /* algorithmic bytes the phase had to read */
+    float kernel_ms;        /* device time of the phase's search launches */
+} boa_phase_stats;
+
+typedef struct {
+    int32_t n_phases;
+    int32_t waves_per_block, blocks; /* launch shape of the first phase */
+    int32_t lds_hash_slots;          /* of the first phase */
+    int64_t spilled_queries;         /* query-phases whose visited set left LDS */
+    float total_ms;                  /* device time of the whole search */
+    boa_phase_stats phase[BOA_MAX_PHASES];
+} boa_stats;
+
+int boa_get_stats(const boa_index *idx, boa_stats *out);
+
+void boa_free_index(boa_index *idx);
+
+const char *boa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BOA_H */

@@ -1,0 +1,195 @@
+"""MI355X-native BOA: batched filtered beam search with online beamwidth
+adaptation ("BOA: Beamwidth Online Adaptation for Filtered-ANNS on a GPU").
+
+Thin ctypes binding of libboa.so (include/boa.h): argument marshalling
+only. Every step of the search runs in the library's HIP kernels; torch
+provides device memory and the stream. Importing this package on a
+machine where libboa.so is not built raises, loudly: there is no CPU
+fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libboa.so")
+
+VEC_F32, VEC_U8 = 0, 1
+ATTR_I32, ATTR_F32 = 0, 1
+PAD = 0xFFFFFFFF
+MAX_PHASES = 32
+ERRORS = {0: "BOA_OK", -1: "BOA_EINVAL", -2: "BOA_ENOMEM", -3: "BOA_EHIP", -4: "BOA_EUNSUPPORTED",
+          -5: "BOA_EOVERFLOW"}
+
+
+class BoaError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class Params(C.Structure):
+    _fields_ = [("k", C.c_int32), ("L0", C.c_int32), ("Lmax", C.c_int32), ("alpha", C.c_double),
+                ("eps", C.c_double), ("tau", C.c_double), ("fixed_L", C.c_int32),
+                ("boa_plus", C.c_int32), ("sub_batches", C.c_int32), ("lds_hash_slots", C.c_int32),
+                ("schedule", C.POINTER(C.c_int32)), ("n_schedule", C.c_int32)]
+
+
+class PhaseStats(C.Structure):
+    _fields_ = [("L", C.c_int32), ("active", C.c_int32), ("confident", C.c_int32),
+                ("launches", C.c_int32), ("expansions", C.c_int64), ("scored", C.c_int64),
+                ("gathered_bytes", C.c_double), ("kernel_ms", C.c_float)]
+
+
+class Stats(C.Structure):
+    _fields_ = [("n_phases", C.c_int32), ("waves_per_block", C.c_int32), ("blocks", C.c_int32),
+                ("lds_hash_slots", C.c_int32), ("spilled_queries", C.c_int64), ("total_ms", C.c_float),
+                ("phase", PhaseStats * MAX_PHASES)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libboa.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                              "(hipcc --offload-arch=gfx950). There is no CPU fallback.")
+        L = C.CDLL(LIB_PATH)
+        P = C.c_void_p
+        L.boa_build_index_from_arrays.restype = C.c_int
+        L.boa_build_index_from_arrays.argtypes = [P, C.c_int64, C.c_int32, C.c_int32, P, C.c_int32, P,
+                                                  P, C.c_int32, C.c_int64, C.POINTER(P)]
+        L.boa_search.restype = C.c_int
+        L.boa_search.argtypes = [P, P, P, C.c_int64, C.POINTER(Params), P, P, P, P, P, P]
+        L.boa_get_stats.restype = C.c_int
+        L.boa_get_stats.argtypes = [P, C.POINTER(Stats)]
+        L.boa_free_index.restype = None
+        L.boa_free_index.argtypes = [P]
+        L.boa_last_error.restype = C.c_char_p
+        L.boa_last_error.argtypes = []
+        L.boa_default_params.restype = None
+        L.boa_default_params.argtypes = [C.POINTER(Params)]
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise BoaError(rc, lib().boa_last_error().decode())
+
+
+def default_params() -> Params:
+    p = Params()
+    lib().boa_default_params(C.byref(p))
+    return p
+
+
+@dataclass
+class SearchResult:
+    ids: "object"        # torch int32 (nq, k); -1 (0xFFFFFFFF) marks padding
+    dists: "object"      # torch float32 (nq, k) squared L2
+    final_L: "object"    # torch int32 (nq,)
+    expansions: "object" = None
+    scored: "object" = None
+
+
+class Index:
+    """A graph index resident in device memory (owned by libboa)."""
+
+    def __init__(self, vectors: np.ndarray, attrs: np.ndarray, attr_dtypes, adjacency: np.ndarray,
+                 entry: int):
+        vectors = np.ascontiguousarray(vectors)
+        if vectors.dtype == np.float32:
+            vt = VEC_F32
+        elif vectors.dtype == np.uint8:
+            vt = VEC_U8
+        else:
+            raise TypeError("vectors must be float32 or uint8")
+        attrs = np.ascontiguousarray(attrs, dtype=np.int32)
+        types = np.ascontiguousarray(attr_dtypes, dtype=np.int32)
+        adj = np.ascontiguousarray(adjacency, dtype=np.uint32)
+        n, d = vectors.shape
+        if attrs.shape != (n, types.shape[0]) or adj.shape[0] != n:
+            raise ValueError("shape mismatch between vectors, attributes and adjacency")
+        h = C.c_void_p()
+        _check(lib().boa_build_index_from_arrays(vectors.ctypes.data, n, d, vt, attrs.ctypes.data,
+                                                 types.shape[0], types.ctypes.data, adj.ctypes.data,
+                                                 adj.shape[1], int(entry), C.byref(h)))
+        self._h = h
+        self.n, self.d, self.m, self.R = n, d, types.shape[0], adj.shape[1]
+        self.vec_dtype = vt
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().boa_free_index(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def search(self, queries, ranges, k: int, L0: int = 16, Lmax: int = 512, alpha: float = 2.0,
+               eps: float = 0.05, tau: float = 0.0, fixed_L: int = 0, boa_plus: bool = False,
+               sub_batches: int = 10, lds_hash_slots: int = 0, schedule=None, counters: bool = False,
+               stream=None, out=None) -> SearchResult:
+        """Adaptive filtered top-k of a batch of device-resident queries.
+
+        queries: torch tensor (nq, d) on the GPU, float32 or uint8 like the index.
+        ranges:  torch int32 tensor (nq, m, 2) on the GPU (float32 columns as bit patterns).
+        """
+        import torch
+        if not (queries.is_cuda and ranges.is_cuda):
+            raise ValueError("queries and ranges must be device tensors")
+        want = torch.float32 if self.vec_dtype == VEC_F32 else torch.uint8
+        if queries.dtype != want or queries.dim() != 2 or queries.shape[1] != self.d:
+            raise ValueError(f"queries must be ({'{'}nq{'}'}, {self.d}) {want}")
+        if ranges.dtype != torch.int32 or tuple(ranges.shape) != (queries.shape[0], self.m, 2):
+            raise ValueError(f"ranges must be int32 of shape (nq, {self.m}, 2)")
+        queries = queries.contiguous()
+        ranges = ranges.contiguous()
+        nq = queries.shape[0]
+        dev = queries.device
+        if out is None:
+            ids = torch.empty((nq, k), dtype=torch.int32, device=dev)
+            dists = torch.empty((nq, k), dtype=torch.float32, device=dev)
+            fl = torch.empty((nq,), dtype=torch.int32, device=dev)
+            E = torch.empty((nq,), dtype=torch.int32, device=dev) if counters else None
+            S = torch.empty((nq,), dtype=torch.int32, device=dev) if counters else None
+        else:
+            ids, dists, fl, E, S = out
+        p = default_params()
+        p.k, p.L0, p.Lmax, p.alpha, p.eps, p.tau = k, L0, Lmax, alpha, eps, tau
+        p.fixed_L, p.boa_plus, p.sub_batches, p.lds_hash_slots = fixed_L, int(boa_plus), sub_batches, lds_hash_slots
+        sched_arr = None
+        if schedule is not None:
+            sched_arr = (C.c_int32 * len(schedule))(*schedule)
+            p.schedule = C.cast(sched_arr, C.POINTER(C.c_int32))
+            p.n_schedule = len(schedule)
+        st = (stream if stream is not None else torch.cuda.current_stream(dev)).cuda_stream
+        _check(lib().boa_search(self._h, queries.data_ptr(), ranges.data_ptr(), nq, C.byref(p),
+                                ids.data_ptr(), dists.data_ptr(), fl.data_ptr(),
+                                E.data_ptr() if E is not None else None,
+                                S.data_ptr() if S is not None else None, st))
+        return SearchResult(ids, dists, fl, E, S)
+
+    def stats(self) -> dict:
+        s = Stats()
+        _check(lib().boa_get_stats(self._h, C.byref(s)))
+        phases = []
+        for i in range(s.n_phases):
+            ph = s.phase[i]
+            phases.append(dict(L=ph.L, active=ph.active, confident=ph.confident, launches=ph.launches,
+                               expansions=ph.expansions, scored=ph.scored,
+                               gathered_bytes=ph.gathered_bytes, kernel_ms=ph.kernel_ms))
+        return dict(phases=phases, waves_per_block=s.waves_per_block, blocks=s.blocks,
+                    lds_hash_slots=s.lds_hash_slots, spilled_queries=s.spilled_queries,
+                    total_ms=s.total_ms)

@@ -1,0 +1,558 @@
+// Host side of libboa: index upload, validation, the multi-phase driver of
+// Alg. 1 (device-side compaction, no host round trip between phases), the
+// BOA+ two-stream schedule, and statistics.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "boa_internal.h"
+
+using namespace boa;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string &msg)
+{
+    g_err = msg;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                  \
+    do {                                                                               \
+        hipError_t e_ = (expr);                                                        \
+        if (e_ != hipSuccess)                                                          \
+            return fail(BOA_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_));  \
+    } while (0)
+
+template <class T>
+int dalloc(T **p, size_t count)
+{
+    *p = nullptr;
+    if (count == 0) count = 1;
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(p), count * sizeof(T));
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        *p = nullptr;
+        return fail(BOA_ENOMEM, "hipMalloc of " + std::to_string(count * sizeof(T)) + " bytes failed");
+    }
+    return BOA_OK;
+}
+
+template <class T>
+void dfree(T *&p)
+{
+    if (p) (void)hipFree(p);
+    p = nullptr;
+}
+
+uint32_t next_pow2(uint64_t x)
+{
+    uint32_t p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+int ilog2(uint32_t x)
+{
+    int r = 0;
+    while ((1u << r) < x) ++r;
+    return r;
+}
+
+struct PhasePlan {
+    int32_t L;
+    int32_t h_slots, wpb, blocks, lds_per_wave;
+    int32_t launches;
+};
+
+}  // namespace
+
+struct boa_index {
+    int device = 0;
+    int num_cu = 0;
+    size_t lds_per_block_max = 65536;
+    int vec_dtype = 0;
+    IndexView view{};
+    void *d_vectors = nullptr;
+    int32_t *d_attrs = nullptr;
+    uint32_t *d_adj = nullptr;
+
+    // workspace, grown on demand
+    int64_t nq_cap = 0;
+    int32_t ph_cap = 0;
+    uint32_t *active[2] = {nullptr, nullptr};
+    uint32_t *n_active = nullptr;    // BOA_MAX_PHASES + 1
+    uint32_t *counters = nullptr;    // work counters, n_counters
+    int32_t n_counters = 0;
+    uint8_t *conf = nullptr;         // nq
+    uint8_t *qstat = nullptr;        // ph_cap x nq
+    uint32_t *qE = nullptr, *qS = nullptr;  // ph_cap x nq
+    uint32_t *status = nullptr;
+    uint32_t *gtab = nullptr;
+    uint32_t *epochs = nullptr;
+    uint64_t slots_cap = 0;
+    int32_t g_log2_cap = 0;
+    uint32_t *pool = nullptr;        // BOA+ survivor pools (ph_cap x nq)
+    hipStream_t aux = nullptr;       // BOA+ second stream
+    std::vector<hipEvent_t> ev_start, ev_end;  // per launch
+
+    // last search
+    int64_t last_nq = 0;
+    int32_t last_k = 0;
+    std::vector<PhasePlan> plans;
+    std::vector<std::pair<int, int>> launch_phase;  // (phase, event index)
+    hipEvent_t ev_all0 = nullptr, ev_all1 = nullptr;
+    bool have_stats = false;
+};
+
+extern "C" {
+
+const char *boa_last_error(void) { return g_err.c_str(); }
+
+void boa_default_params(boa_params *p)
+{
+    if (!p) return;
+    std::memset(p, 0, sizeof(*p));
+    p->k = 10;
+    p->L0 = 16;
+    p->Lmax = 512;
+    p->alpha = 2.0;
+    p->eps = 0.05;
+    p->tau = 0.0;
+    p->fixed_L = 0;
+    p->boa_plus = 0;
+    p->sub_batches = 10;
+    p->lds_hash_slots = 0;
+    p->schedule = nullptr;
+    p->n_schedule = 0;
+}
+
+void boa_free_index(boa_index *ix)
+{
+    if (!ix) return;
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(ix->device);
+    dfree(ix->d_vectors);
+    dfree(ix->d_attrs);
+    dfree(ix->d_adj);
+    dfree(ix->active[0]);
+    dfree(ix->active[1]);
+    dfree(ix->n_active);
+    dfree(ix->counters);
+    dfree(ix->conf);
+    dfree(ix->qstat);
+    dfree(ix->qE);
+    dfree(ix->qS);
+    dfree(ix->status);
+    dfree(ix->gtab);
+    dfree(ix->epochs);
+    dfree(ix->pool);
+    for (auto e : ix->ev_start) (void)hipEventDestroy(e);
+    for (auto e : ix->ev_end) (void)hipEventDestroy(e);
+    if (ix->ev_all0) (void)hipEventDestroy(ix->ev_all0);
+    if (ix->ev_all1) (void)hipEventDestroy(ix->ev_all1);
+    if (ix->aux) (void)hipStreamDestroy(ix->aux);
+    (void)hipSetDevice(cur);
+    delete ix;
+}
+
+int boa_build_index_from_arrays(const void *vectors, int64_t n, int32_t d, int32_t vec_dtype,
+                                const int32_t *attrs, int32_t m, const int32_t *attr_dtypes,
+                                const uint32_t *adjacency, int32_t R, int64_t entry, boa_index **out)
+{
+    if (!out) return fail(BOA_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!vectors || !attrs || !attr_dtypes) return fail(BOA_EINVAL, "NULL input array");
+    if (!adjacency)
+        return fail(BOA_EUNSUPPORTED, "graph construction is not part of this library; pass an adjacency");
+    if (n < 1 || n >= BOA_MAX_N) return fail(BOA_EINVAL, "n out of range [1, 2^24)");
+    if (vec_dtype != BOA_VEC_F32 && vec_dtype != BOA_VEC_U8) return fail(BOA_EINVAL, "bad vec_dtype");
+    if (d < 4 || d > 1024) return fail(BOA_EINVAL, "d out of range [4, 1024]");
+    if (vec_dtype == BOA_VEC_F32 && d % 4) return fail(BOA_EINVAL, "float32 vectors need d % 4 == 0");
+    if (vec_dtype == BOA_VEC_U8 && d % 16) return fail(BOA_EINVAL, "uint8 vectors need d % 16 == 0");
+    if (m < 1 || m > BOA_MAX_M) return fail(BOA_EINVAL, "m out of range [1, 8]");
+    if (R < 1 || R > BOA_MAX_R) return fail(BOA_EINVAL, "R out of range [1, 64]");
+    if (entry < 0 || entry >= n) return fail(BOA_EINVAL, "entry out of range");
+    uint32_t f32_mask = 0;
+    for (int j = 0; j < m; ++j) {
+        if (attr_dtypes[j] == BOA_ATTR_F32) f32_mask |= 1u << j;
+        else if (attr_dtypes[j] != BOA_ATTR_I32) return fail(BOA_EINVAL, "bad attribute dtype");
+    }
+    for (int64_t i = 0; i < n * (int64_t)R; ++i) {
+        uint32_t v = adjacency[i];
+        if (v != BOA_PAD && (int64_t)v >= n) return fail(BOA_EINVAL, "adjacency id out of range");
+        if (v != BOA_PAD && (int64_t)v == i / R) return fail(BOA_EINVAL, "adjacency row holds its own id");
+    }
+
+    boa_index *ix = new (std::nothrow) boa_index();
+    if (!ix) return fail(BOA_ENOMEM, "host allocation failed");
+    if (hipGetDevice(&ix->device) != hipSuccess) {
+        delete ix;
+        return fail(BOA_EHIP, "hipGetDevice failed (no GPU?)");
+    }
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, ix->device) != hipSuccess) {
+        delete ix;
+        return fail(BOA_EHIP, "hipGetDeviceProperties failed");
+    }
+    ix->num_cu = prop.multiProcessorCount;
+    ix->lds_per_block_max = std::min<size_t>(prop.sharedMemPerBlock, 65536);
+    ix->vec_dtype = vec_dtype;
+
+    const int m_pad = m <= 1 ? 1 : (m <= 2 ? 2 : (m <= 4 ? 4 : 8));
+    const size_t esz = vec_dtype == BOA_VEC_U8 ? 1 : 4;
+    int rc;
+    if ((rc = dalloc(reinterpret_cast<uint8_t **>(&ix->d_vectors), (size_t)n * d * esz)) ||
+        (rc = dalloc(&ix->d_attrs, (size_t)n * m_pad)) || (rc = dalloc(&ix->d_adj, (size_t)n * R))) {
+        boa_free_index(ix);
+        return rc;
+    }
+    std::vector<int32_t> padded;
+    const int32_t *attr_src = attrs;
+    if (m_pad != m) {
+        try {
+            padded.assign((size_t)n * m_pad, 0);
+        } catch (...) {
+            boa_free_index(ix);
+            return fail(BOA_ENOMEM, "host allocation failed");
+        }
+        for (int64_t i = 0; i < n; ++i)
+            std::memcpy(&padded[(size_t)i * m_pad], attrs + (size_t)i * m, sizeof(int32_t) * m);
+        attr_src = padded.data();
+    }
+    if (hipMemcpy(ix->d_vectors, vectors, (size_t)n * d * esz, hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(ix->d_attrs, attr_src, (size_t)n * m_pad * 4, hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(ix->d_adj, adjacency, (size_t)n * R * 4, hipMemcpyHostToDevice) != hipSuccess) {
+        boa_free_index(ix);
+        return fail(BOA_EHIP, "index upload failed");
+    }
+    ix->view.vectors = ix->d_vectors;
+    ix->view.attrs = ix->d_attrs;
+    ix->view.adj = ix->d_adj;
+    ix->view.n = n;
+    ix->view.d = d;
+    ix->view.m = m;
+    ix->view.m_pad = m_pad;
+    ix->view.R = R;
+    ix->view.entry = (uint32_t)entry;
+    ix->view.f32_mask = f32_mask;
+    if (hipEventCreate(&ix->ev_all0) != hipSuccess || hipEventCreate(&ix->ev_all1) != hipSuccess) {
+        boa_free_index(ix);
+        return fail(BOA_EHIP, "hipEventCreate failed");
+    }
+    *out = ix;
+    return BOA_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+int ensure_events(boa_index *ix, size_t count)
+{
+    while (ix->ev_start.size() < count) {
+        hipEvent_t a, b;
+        HIP_TRY(hipEventCreate(&a));
+        HIP_TRY(hipEventCreate(&b));
+        ix->ev_start.push_back(a);
+        ix->ev_end.push_back(b);
+    }
+    return BOA_OK;
+}
+
+int ensure_workspace(boa_index *ix, int64_t nq, int32_t n_phases, uint64_t slots, int32_t g_log2,
+                     int32_t n_counters, bool plus)
+{
+    int rc;
+    if (nq > ix->nq_cap || n_phases > ix->ph_cap) {
+        int64_t cap = std::max<int64_t>(nq, ix->nq_cap);
+        int32_t pc = std::max<int32_t>(n_phases, ix->ph_cap);
+        dfree(ix->active[0]);
+        dfree(ix->active[1]);
+        dfree(ix->conf);
+        dfree(ix->qstat);
+        dfree(ix->qE);
+        dfree(ix->qS);
+        dfree(ix->pool);
+        if ((rc = dalloc(&ix->active[0], cap)) || (rc = dalloc(&ix->active[1], cap)) ||
+            (rc = dalloc(&ix->conf, cap)) || (rc = dalloc(&ix->qstat, (size_t)cap * pc)) ||
+            (rc = dalloc(&ix->qE, (size_t)cap * pc)) || (rc = dalloc(&ix->qS, (size_t)cap * pc)) ||
+            (rc = dalloc(&ix->pool, (size_t)cap * pc))) {
+            ix->nq_cap = 0;
+            ix->ph_cap = 0;
+            return rc;
+        }
+        ix->nq_cap = cap;
+        ix->ph_cap = pc;
+    }
+    if (!ix->n_active) {
+        if ((rc = dalloc(&ix->n_active, 2 * (BOA_MAX_PHASES + 1)))) return rc;
+        if ((rc = dalloc(&ix->status, 16))) return rc;
+    }
+    if (n_counters > ix->n_counters) {
+        dfree(ix->counters);
+        if ((rc = dalloc(&ix->counters, n_counters))) return rc;
+        ix->n_counters = n_counters;
+    }
+    if (slots > ix->slots_cap || g_log2 > ix->g_log2_cap) {
+        uint64_t sc = std::max<uint64_t>(slots, ix->slots_cap);
+        int32_t gl = std::max<int32_t>(g_log2, ix->g_log2_cap);
+        dfree(ix->gtab);
+        dfree(ix->epochs);
+        if ((rc = dalloc(&ix->gtab, (size_t)sc << gl)) || (rc = dalloc(&ix->epochs, sc))) {
+            ix->slots_cap = 0;
+            ix->g_log2_cap = 0;
+            return rc;
+        }
+        HIP_TRY(hipMemset(ix->gtab, 0, ((size_t)sc << gl) * sizeof(uint32_t)));
+        HIP_TRY(hipMemset(ix->epochs, 0, sc * sizeof(uint32_t)));
+        ix->slots_cap = sc;
+        ix->g_log2_cap = gl;
+    }
+    if (plus && !ix->aux) HIP_TRY(hipStreamCreateWithFlags(&ix->aux, hipStreamNonBlocking));
+    return BOA_OK;
+}
+
+// Beam schedule: L_{p+1} = min(ceil(alpha * L_p), Lmax); the phase at Lmax is the last.
+int make_schedule(const boa_params *p, std::vector<int32_t> &s)
+{
+    s.clear();
+    if (p->fixed_L > 0) {
+        s.push_back(p->fixed_L);
+        return BOA_OK;
+    }
+    if (p->schedule && p->n_schedule > 0) {
+        for (int i = 0; i < p->n_schedule; ++i) {
+            if (p->schedule[i] < 1 || (i && p->schedule[i] <= p->schedule[i - 1]))
+                return fail(BOA_EINVAL, "schedule must be positive and strictly increasing");
+            s.push_back(p->schedule[i]);
+        }
+        if ((int)s.size() > BOA_MAX_PHASES) return fail(BOA_EINVAL, "too many phases");
+        return BOA_OK;
+    }
+    if (!(p->alpha > 1.0) || !std::isfinite(p->alpha)) return fail(BOA_EINVAL, "alpha must be > 1");
+    if (p->L0 < 1 || p->Lmax < p->L0) return fail(BOA_EINVAL, "need 1 <= L0 <= Lmax");
+    int64_t L = p->L0;
+    for (;;) {
+        if ((int)s.size() >= BOA_MAX_PHASES) return fail(BOA_EINVAL, "schedule exceeds BOA_MAX_PHASES");
+        s.push_back((int32_t)L);
+        if (L >= p->Lmax) break;
+        int64_t nx = (int64_t)std::ceil(p->alpha * (double)L);
+        if (nx <= L) nx = L + 1;
+        L = nx < p->Lmax ? nx : p->Lmax;
+    }
+    return BOA_OK;
+}
+
+PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t max_active)
+{
+    PhasePlan pl{};
+    pl.L = L;
+    uint32_t h = forced_h > 0 ? (uint32_t)forced_h
+                              : std::min<uint32_t>(8192u, std::max<uint32_t>(2048u, next_pow2(32ull * L)));
+    pl.h_slots = (int32_t)h;
+    pl.lds_per_wave = (int32_t)(8 * L + 64 * (8 + 4 + 4 + 4) + 4 * h);
+    pl.lds_per_wave = (pl.lds_per_wave + 15) & ~15;
+    int wpb = 4;
+    while (wpb > 1 && (size_t)wpb * pl.lds_per_wave > ix->lds_per_block_max) wpb >>= 1;
+    pl.wpb = wpb;
+    int occ = phase_occupancy(ix->vec_dtype, ix->view.d, wpb, (size_t)wpb * pl.lds_per_wave);
+    if (occ < 1) occ = 1;
+    int64_t blocks = (int64_t)occ * ix->num_cu;
+    int64_t need = (max_active + wpb - 1) / wpb;
+    if (need < 1) need = 1;
+    pl.blocks = (int32_t)std::min<int64_t>(blocks, need);
+    pl.launches = 0;
+    return pl;
+}
+
+}  // namespace
+
+extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_t nq,
+                          const boa_params *p, uint32_t *ids, float *dists, int32_t *final_L,
+                          uint32_t *expansions, uint32_t *scored, void *stream_v)
+{
+    if (!ix || !p) return fail(BOA_EINVAL, "NULL index or params");
+    if (nq < 0 || nq >= (int64_t)1 << 31) return fail(BOA_EINVAL, "nq out of range");
+    if (nq > 0 && (!queries || !ranges || !ids || !dists || !final_L))
+        return fail(BOA_EINVAL, "NULL device buffer");
+    std::vector<int32_t> sched;
+    int rc = make_schedule(p, sched);
+    if (rc) return rc;
+    for (int32_t L : sched)
+        if (L < 1 || L > BOA_MAX_L) return fail(BOA_EINVAL, "beamwidth out of range [1, 2048]");
+    if (p->k < 1 || p->k > sched[0]) return fail(BOA_EINVAL, "need 1 <= k <= first-phase beamwidth");
+    if (!(p->eps >= 0.0) || !std::isfinite(p->eps)) return fail(BOA_EINVAL, "eps must be >= 0");
+    if (!(p->tau >= 0.0 && p->tau < 1.0)) return fail(BOA_EINVAL, "tau must be in [0, 1)");
+    if (p->lds_hash_slots && (p->lds_hash_slots < 64 || (p->lds_hash_slots & (p->lds_hash_slots - 1)) ||
+                              p->lds_hash_slots > 16384))
+        return fail(BOA_EINVAL, "lds_hash_slots must be 0 or a power of two in [64, 16384]");
+    if (p->lds_hash_slots && (uint32_t)p->lds_hash_slots / 2 < (uint32_t)ix->view.R + 1)
+        return fail(BOA_EINVAL, "lds_hash_slots too small for the graph degree");
+    const bool plus = p->boa_plus != 0 && p->fixed_L <= 0;
+    if (plus && (p->sub_batches < 1 || p->sub_batches > 1024)) return fail(BOA_EINVAL, "sub_batches out of range");
+    if (nq == 0) return BOA_OK;
+
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream_v);
+    int cur_dev = 0;
+    HIP_TRY(hipGetDevice(&cur_dev));
+    if (cur_dev != ix->device) return fail(BOA_EINVAL, "index lives on another device than the current one");
+
+    const int32_t n_phases = (int32_t)sched.size();
+    std::vector<PhasePlan> plans;
+    uint64_t slots = 0;
+    for (int32_t ph = 0; ph < n_phases; ++ph) {
+        PhasePlan pl = plan_phase(ix, sched[ph], p->lds_hash_slots, nq);
+        if ((size_t)pl.lds_per_wave > ix->lds_per_block_max)
+            return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
+        slots = std::max<uint64_t>(slots, (uint64_t)pl.blocks * pl.wpb);
+        plans.push_back(pl);
+    }
+    const int32_t Lmax = sched.back();
+    int32_t g_log2 = ilog2(std::min<uint32_t>(1u << 20, std::max<uint32_t>(1u << 14, next_pow2(64ull * Lmax))));
+    const int32_t sub = plus ? std::min<int32_t>(p->sub_batches, (int32_t)nq) : 1;
+    const int32_t n_counters = n_phases * (sub + 1) + 8;
+    if ((rc = ensure_workspace(ix, nq, n_phases, plus ? 2 * slots : slots, g_log2, n_counters, plus))) return rc;
+    if ((rc = ensure_events(ix, (size_t)n_phases * (sub + 1)))) return rc;
+    const uint32_t tau_count = (uint32_t)std::floor(p->tau * (double)nq);
+
+    InitArgs ia{};
+    ia.active0 = ix->active[0];
+    ia.n_active = ix->n_active;
+    ia.counters = ix->counters;
+    ia.qstat = ix->qstat;
+    ia.user_E = expansions;
+    ia.user_S = scored;
+    ia.status = ix->status;
+    ia.nq = nq;
+    ia.n_phases = n_phases;
+    ia.n_counters = n_counters;
+
+    ix->launch_phase.clear();
+    ix->have_stats = false;
+    HIP_TRY(hipEventRecord(ix->ev_all0, st));
+    HIP_TRY(launch_init(ia, st));
+
+    PhaseArgs base{};
+    base.ix = ix->view;
+    base.queries = queries;
+    base.ranges = ranges;
+    base.ids = ids;
+    base.dists = dists;
+    base.final_L = final_L;
+    base.user_E = expansions;
+    base.user_S = scored;
+    base.gtab = ix->gtab;
+    base.epochs = ix->epochs;
+    base.status = ix->status;
+    base.eps = p->eps;
+    base.tau_count = tau_count;
+    base.k = p->k;
+    base.g_log2 = ix->g_log2_cap;
+    base.conf = ix->conf;
+    int ev = 0;
+
+    if (!plus) {
+        for (int32_t ph = 0; ph < n_phases; ++ph) {
+            PhasePlan &pl = plans[ph];
+            PhaseArgs a = base;
+            a.active = ix->active[ph & 1];
+            a.n_active = ix->n_active + ph;
+            a.t_begin = 0;
+            a.t_end = 0xFFFFFFFFu;
+            a.queue = ix->counters + ph;
+            a.qstat = ix->qstat + (size_t)ph * nq;
+            a.qE = ix->qE + (size_t)ph * nq;
+            a.qS = ix->qS + (size_t)ph * nq;
+            a.L = pl.L;
+            a.h_log2 = ilog2((uint32_t)pl.h_slots);
+            a.lds_per_wave = pl.lds_per_wave;
+            a.waves_per_block = pl.wpb;
+            a.slot_base = 0;
+            HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
+            HIP_TRY(launch_phase(a, ix->vec_dtype, pl.blocks, st));
+            HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
+            ix->launch_phase.push_back({ph, ev});
+            ++ev;
+            pl.launches = 1;
+            if (ph + 1 < n_phases) {
+                CompactArgs ca{};
+                ca.in = ix->active[ph & 1];
+                ca.n_in = ix->n_active + ph;
+                ca.conf = ix->conf;
+                ca.out = ix->active[(ph + 1) & 1];
+                ca.n_out = ix->n_active + ph + 1;
+                ca.tau_count = tau_count;
+                HIP_TRY(launch_compact(ca, st));
+            }
+        }
+    } else {
+        return fail(BOA_EUNSUPPORTED, "BOA+ is not available in this build yet");
+    }
+
+    HIP_TRY(hipEventRecord(ix->ev_all1, st));
+    uint32_t status = 0;
+    HIP_TRY(hipMemcpyAsync(&status, ix->status, sizeof(uint32_t), hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    ix->plans = plans;
+    ix->last_nq = nq;
+    ix->last_k = p->k;
+    ix->have_stats = true;
+    if (status & BOA_STATUS_OVERFLOW)
+        return fail(BOA_EOVERFLOW, "a visited table overflowed; results are not valid");
+    return BOA_OK;
+}
+
+extern "C" int boa_get_stats(const boa_index *ix, boa_stats *out)
+{
+    if (!ix || !out) return fail(BOA_EINVAL, "NULL argument");
+    std::memset(out, 0, sizeof(*out));
+    if (!ix->have_stats) return fail(BOA_EINVAL, "no completed search on this index");
+    const int64_t nq = ix->last_nq;
+    const int32_t np = (int32_t)ix->plans.size();
+    out->n_phases = np;
+    out->waves_per_block = ix->plans[0].wpb;
+    out->blocks = ix->plans[0].blocks;
+    out->lds_hash_slots = ix->plans[0].h_slots;
+    std::vector<uint8_t> st((size_t)nq * np);
+    std::vector<uint32_t> E((size_t)nq * np), S((size_t)nq * np);
+    HIP_TRY(hipMemcpy(st.data(), ix->qstat, st.size(), hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(E.data(), ix->qE, E.size() * 4, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(S.data(), ix->qS, S.size() * 4, hipMemcpyDeviceToHost));
+    const IndexView &v = ix->view;
+    const double e = ix->vec_dtype == BOA_VEC_U8 ? 1.0 : 4.0;
+    for (int32_t ph = 0; ph < np; ++ph) {
+        boa_phase_stats &ps = out->phase[ph];
+        ps.L = ix->plans[ph].L;
+        ps.launches = ix->plans[ph].launches;
+        for (int64_t i = 0; i < nq; ++i) {
+            uint8_t s = st[(size_t)ph * nq + i];
+            if (!s) continue;
+            ps.active += 1;
+            ps.confident += (s & 3u) == 2u;
+            out->spilled_queries += (s & 4u) != 0;
+            ps.expansions += E[(size_t)ph * nq + i];
+            ps.scored += S[(size_t)ph * nq + i];
+        }
+        ps.gathered_bytes = 4.0 * v.R * (double)ps.expansions + (4.0 * v.m + v.d * e) * (double)ps.scored +
+                            (v.d * e + 8.0 * v.m + 8.0 * ix->last_k + 4.0) * (double)ps.active;
+    }
+    for (auto &lp : ix->launch_phase) {
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, ix->ev_start[lp.second], ix->ev_end[lp.second]));
+        out->phase[lp.first].kernel_ms += ms;
+    }
+    float tot = 0.f;
+    HIP_TRY(hipEventElapsedTime(&tot, ix->ev_all0, ix->ev_all1));
+    out->total_ms = tot;
+    return BOA_OK;
+}

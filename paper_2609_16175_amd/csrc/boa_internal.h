@@ -1,0 +1,78 @@
+// Internal types shared by the host driver and the kernels of libboa.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "boa.h"
+
+#define BOA_PAD 0xFFFFFFFFu
+#define BOA_STATUS_OVERFLOW 1u
+
+namespace boa {
+
+// Device-resident index. Attribute rows are padded to m_pad in {1, 2, 4, 8}
+// cells so one aligned vector load fetches a whole record.
+struct IndexView {
+    const void *vectors;      // n x d (float32 or uint8)
+    const int32_t *attrs;     // n x m_pad cells
+    const uint32_t *adj;      // n x R
+    int64_t n;
+    int32_t d, m, m_pad, R;
+    uint32_t entry;
+    uint32_t f32_mask;        // bit j set: attribute j is float32
+};
+
+struct PhaseArgs {
+    IndexView ix;
+    const void *queries;      // nq x d
+    const int32_t *ranges;    // nq x m x 2
+    const uint32_t *active;   // active list of this phase (query indices)
+    const uint32_t *n_active; // its length (device)
+    uint32_t t_begin, t_end;  // slice of the active list served by this launch
+    uint32_t *queue;          // work counter of this launch
+    uint8_t *conf;            // per active slot: confident flag
+    uint32_t *ids;
+    float *dists;
+    int32_t *final_L;
+    uint8_t *qstat;           // per query, this phase: 0 not run, 1 ran, 2 ran+confident, +4 spilled
+    uint32_t *qE, *qS;        // per query, this phase: expansions, scored
+    uint32_t *user_E, *user_S;// optional per-query totals over phases
+    uint32_t *gtab;           // visited spill tables, (1 << g_log2) entries per wave slot
+    uint32_t *epochs;         // per wave slot
+    uint32_t *status;
+    double eps;
+    uint32_t tau_count;       // the phase runs only if n_active > tau_count
+    int32_t L, k;
+    int32_t h_log2, g_log2;
+    int32_t lds_per_wave, waves_per_block;
+    uint32_t slot_base;
+};
+
+struct CompactArgs {
+    const uint32_t *in;
+    const uint32_t *n_in;
+    const uint8_t *conf;
+    uint32_t *out;
+    uint32_t *n_out;
+    uint32_t tau_count;
+};
+
+struct InitArgs {
+    uint32_t *active0;
+    uint32_t *n_active;
+    uint32_t *counters;
+    uint8_t *qstat;
+    uint32_t *user_E, *user_S;
+    uint32_t *status;
+    int64_t nq;
+    int32_t n_phases;
+    int32_t n_counters;
+};
+
+hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st);
+int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds);
+hipError_t launch_compact(const CompactArgs &a, hipStream_t st);
+hipError_t launch_init(const InitArgs &a, hipStream_t st);
+
+}  // namespace boa

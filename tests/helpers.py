@@ -1,0 +1,104 @@
+"""Shared test helpers: small random indexes and independent numpy checks."""
+import numpy as np
+
+import oracle
+from workloads import gen
+
+PAD = 0xFFFFFFFF
+I32_MIN, I32_MAX = -2**31, 2**31 - 1
+
+
+def ring_knn_graph(x: np.ndarray, R: int, seed: int) -> np.ndarray:
+    """kNN rows (float64) with the last slot pointing to i+1: strongly connected."""
+    n = x.shape[0]
+    xf = x.astype(np.float64)
+    sq = (xf * xf).sum(1)
+    d = sq[:, None] + sq[None, :] - 2.0 * (xf @ xf.T)
+    np.fill_diagonal(d, np.inf)
+    order = np.argsort(d, axis=1, kind="stable")[:, :R - 1]
+    adj = np.full((n, R), PAD, dtype=np.uint32)
+    adj[:, :R - 1] = order
+    rng = np.random.default_rng(seed)
+    # knock out a few slots to exercise padding in the middle of rows
+    holes = rng.random((n, R - 1)) < 0.1
+    adj[:, :R - 1][holes] = PAD
+    nxt = (np.arange(n) + 1) % n
+    for i in range(n):
+        if nxt[i] not in adj[i, :R - 1]:
+            adj[i, R - 1] = nxt[i]
+    return adj
+
+
+def random_arrays(n=400, d=16, m=2, R=12, dtype="f32", seed=0, f32_col=False):
+    """(vectors, attrs, attr_dtypes, adjacency, entry) of a small random index."""
+    rng = np.random.default_rng(seed)
+    if dtype == "u8":
+        x = rng.integers(0, 256, size=(n, d)).astype(np.uint8)
+    else:
+        c = rng.normal(size=(4, d))
+        x = (c[rng.integers(0, 4, n)] + 0.5 * rng.normal(size=(n, d))).astype(np.float32)
+    attrs = rng.integers(0, 100, size=(n, m)).astype(np.int32)
+    types = np.zeros(m, dtype=np.int32)
+    if f32_col:
+        types[-1] = gen.ATTR_F32
+        attrs[:, -1] = gen.f32_bits(rng.normal(size=n).astype(np.float32))
+    adj = ring_knn_graph(x, R, seed)
+    return x, attrs, types, adj, int(rng.integers(0, n))
+
+
+def random_index(**kw):
+    return oracle.Index(*random_arrays(**kw))
+
+
+def random_queries(ix, nq, sel_width, seed, f32_col=False):
+    rng = np.random.default_rng(seed + 1)
+    n, d = ix.vectors.shape
+    if ix.vectors.dtype == np.uint8:
+        q = rng.integers(0, 256, size=(nq, d)).astype(np.uint8)
+    else:
+        q = ix.vectors[rng.integers(0, n, nq)] + 0.3 * rng.normal(size=(nq, d)).astype(np.float32)
+        q = q.astype(np.float32)
+    r = np.zeros((nq, ix.m, 2), dtype=np.int32)
+    lo = rng.integers(0, 100 - sel_width + 1, size=(nq, ix.m))
+    r[:, :, 0] = lo
+    r[:, :, 1] = lo + sel_width - 1
+    if f32_col:
+        a = rng.normal(size=(nq, 2)).astype(np.float32)
+        r[:, -1, 0] = gen.f32_bits(np.minimum(a[:, 0], a[:, 1]))
+        r[:, -1, 1] = gen.f32_bits(np.maximum(a[:, 0], a[:, 1]) + 0.5)
+    return q, r
+
+
+def numpy_valid(ix, r):
+    """Eq. 2 evaluated with numpy, column by column in its own type."""
+    ok = np.ones(ix.n, dtype=bool)
+    for j in range(ix.m):
+        if ix.attr_dtypes[j] == gen.ATTR_F32:
+            a = gen.cells_as_f32(ix.attrs[:, j])
+            lo, hi = gen.cells_as_f32(r[j:j + 1, 0])[0], gen.cells_as_f32(r[j:j + 1, 1])[0]
+        else:
+            a, lo, hi = ix.attrs[:, j], r[j, 0], r[j, 1]
+        ok &= (lo <= a) & (a <= hi)
+    return ok
+
+
+def numpy_filtered_topk(ix, q, r, k):
+    """Def. 1 with float64 distances: (ids, d64) of the k nearest valid points."""
+    ok = np.flatnonzero(numpy_valid(ix, r))
+    d = ((ix.vectors[ok].astype(np.float64) - q.astype(np.float64)) ** 2).sum(1)
+    o = np.lexsort((ok, d))[:k]
+    return ok[o], d[o]
+
+
+def assert_same_up_to_near_ties(ids, dists, ref_ids, ref_d64, rel=1e-5):
+    """ids equal except where float rounding can swap near-tied neighbours."""
+    valid = ids != PAD
+    assert valid.sum() == len(ref_ids)
+    np.testing.assert_allclose(dists[valid], ref_d64, rtol=1e-5, atol=1e-6)
+    for j, (a, b) in enumerate(zip(ids[valid], ref_ids)):
+        if a != b:
+            # allowed only if a tie partner sits within rel of position j
+            near = np.abs(ref_d64 - ref_d64[j]) <= rel * max(ref_d64[j], 1e-30)
+            assert a in set(ref_ids[near]) or near.sum() > 1, (j, a, b)
+
+

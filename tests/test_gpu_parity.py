@@ -1,0 +1,196 @@
+"""GPU parity: the HIP search (through the C ABI) against the CPU oracle.
+
+Bar: ids, distances, final widths and per-query expansion/scored counts
+identical to the oracle (both sides use one float32 summation order and
+take every decision in the same precision), on seeded inputs spanning
+several wave rounds, ragged candidate counts and the edge cases.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import PAD, random_arrays, random_queries
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _boa():
+    import paper_2609_16175_amd as boa
+    return boa
+
+
+def gpu_search(ix, q, r, **kw):
+    dev = torch.device("cuda:0")
+    qt = torch.from_numpy(np.ascontiguousarray(q)).to(dev)
+    rt = torch.from_numpy(np.ascontiguousarray(r, dtype=np.int32)).to(dev)
+    out = ix.search(qt, rt, counters=True, **kw)
+    torch.cuda.synchronize()
+    return (out.ids.cpu().numpy().view(np.uint32), out.dists.cpu().numpy(), out.final_L.cpu().numpy(),
+            out.expansions.cpu().numpy().astype(np.int64), out.scored.cpu().numpy().astype(np.int64))
+
+
+def assert_parity(got, ref, what=""):
+    ids, dists, fl, E, S = got
+    bad = np.flatnonzero((ids != ref.ids).any(1) | (dists != ref.dists).any(1) | (fl != ref.final_L)
+                         | (E != ref.expansions) | (S != ref.scored))
+    if bad.size:
+        i = bad[0]
+        raise AssertionError(
+            f"{what}: {bad.size} queries differ; first {i}: gpu ids {ids[i]} oracle {ref.ids[i]}; "
+            f"gpu d {dists[i]} oracle {ref.dists[i]}; L {fl[i]} vs {ref.final_L[i]}; "
+            f"E {E[i]} vs {ref.expansions[i]}; S {S[i]} vs {ref.scored[i]}")
+
+
+# ---------------------------------------------------------------------------
+# the tiny workload: 10k points, d=32, R=16, m=1, 100 queries, L 16 -> 128
+
+@pytest.fixture(scope="module")
+def tiny():
+    from workloads import gen, graph
+    wl = gen.TINY
+    data = gen.generate(wl)
+    adj, entry = graph.build_graph(data.vectors, wl.R, "cpu")
+    types = np.array(wl.attr_dtypes, dtype=np.int32)
+    boa = _boa()
+    return dict(wl=wl, data=data, orc=oracle.Index(data.vectors, data.attrs, types, adj, entry),
+                gpu=boa.Index(data.vectors, data.attrs, types, adj, entry))
+
+
+def test_tiny_adaptive(tiny):
+    wl, d = tiny["wl"], tiny["data"]
+    sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
+    ref = oracle.boa(tiny["orc"], d.queries, d.ranges, wl.k, sched)
+    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax)
+    assert_parity(got, ref, "tiny adaptive")
+    st = tiny["gpu"].stats()
+    assert [p["L"] for p in st["phases"]] == sched
+    for p, rp in zip(st["phases"], ref.phases):
+        assert (p["active"], p["confident"], p["expansions"], p["scored"]) == \
+            (rp["active"], rp["confident"], rp["expansions"], rp["scored"])
+
+
+@pytest.mark.parametrize("L", [10, 16, 64, 128, 500])
+def test_tiny_fixed_width(tiny, L):
+    wl, d = tiny["wl"], tiny["data"]
+    ref = oracle.boa(tiny["orc"], d.queries, d.ranges, wl.k, [L])
+    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, fixed_L=L)
+    assert_parity(got, ref, f"tiny fixed L={L}")
+
+
+@pytest.mark.parametrize("slots", [64, 256])
+def test_forced_spill_changes_nothing(tiny, slots):
+    """A tiny LDS visited table sends almost every insert to the HBM table."""
+    wl, d = tiny["wl"], tiny["data"]
+    sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
+    ref = oracle.boa(tiny["orc"], d.queries, d.ranges, wl.k, sched)
+    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax,
+                     lds_hash_slots=slots)
+    assert_parity(got, ref, f"spill slots={slots}")
+    assert tiny["gpu"].stats()["spilled_queries"] > 0
+    # and twice in a row: the wave-slot epochs must isolate the searches
+    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax,
+                     lds_hash_slots=slots)
+    assert_parity(got, ref, f"spill slots={slots}, repeated")
+
+
+def test_paper_schedule(tiny):
+    """The paper's experiments use widths 10, 100, 200 (Sec. IV)."""
+    wl, d = tiny["wl"], tiny["data"]
+    ref = oracle.boa(tiny["orc"], d.queries, d.ranges, 10, [10, 100, 200], eps=0.02)
+    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=10, schedule=[10, 100, 200], eps=0.02)
+    assert_parity(got, ref, "schedule 10/100/200")
+
+
+def test_single_query_equals_batch(tiny):
+    wl, d = tiny["wl"], tiny["data"]
+    full = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax)
+    for i in (0, 37, 99):
+        one = gpu_search(tiny["gpu"], d.queries[i:i + 1], d.ranges[i:i + 1], k=wl.k, L0=wl.L0, Lmax=wl.Lmax)
+        for a, b in zip(one, full):
+            np.testing.assert_array_equal(a[0], b[i])
+
+
+def test_tau_residual(tiny):
+    wl, d = tiny["wl"], tiny["data"]
+    sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
+    for tau in (0.01, 0.05, 0.5):
+        ref = oracle.boa(tiny["orc"], d.queries, d.ranges, wl.k, sched, eps=0.2, tau=tau)
+        got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax, eps=0.2, tau=tau)
+        assert_parity(got, ref, f"tau={tau}")
+
+
+def test_k_equal_first_width_and_k_one(tiny):
+    wl, d = tiny["wl"], tiny["data"]
+    for k, L0 in ((16, 16), (1, 16), (10, 10)):
+        sched = oracle.schedule(L0, 2.0, 128)
+        ref = oracle.boa(tiny["orc"], d.queries, d.ranges, k, sched)
+        got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=k, L0=L0, Lmax=128)
+        assert_parity(got, ref, f"k={k} L0={L0}")
+
+
+def test_empty_valid_sets_and_unbounded(tiny):
+    wl, d = tiny["wl"], tiny["data"]
+    r = d.ranges.copy()
+    r[::3, 0] = [5000, 6000]                      # nothing valid
+    r[1::3, 0] = [-2**31, 2**31 - 1]              # everything valid
+    sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
+    ref = oracle.boa(tiny["orc"], d.queries, r, wl.k, sched)
+    got = gpu_search(tiny["gpu"], d.queries, r, k=wl.k, L0=wl.L0, Lmax=wl.Lmax)
+    assert_parity(got, ref, "empty/unbounded ranges")
+    assert (got[0][::3] == PAD).all() and np.isinf(got[1][::3]).all()
+
+
+def test_no_queries(tiny):
+    boa = _boa()
+    q = torch.zeros((0, 32), dtype=torch.float32, device="cuda:0")
+    r = torch.zeros((0, 1, 2), dtype=torch.int32, device="cuda:0")
+    out = tiny["gpu"].search(q, r, k=10)
+    assert out.ids.shape == (0, 10)
+    with pytest.raises(boa.BoaError):
+        tiny["gpu"].search(q, r, k=20, L0=16)          # k above the first width
+    with pytest.raises(boa.BoaError):
+        tiny["gpu"].search(q, r, k=10, Lmax=4096)       # beyond the widest supported width
+    with pytest.raises(boa.BoaError):
+        tiny["gpu"].search(q, r, k=10, tau=1.0)
+    with pytest.raises(boa.BoaError):
+        tiny["gpu"].search(q, r, k=10, lds_hash_slots=100)
+
+
+# ---------------------------------------------------------------------------
+# shapes: float32 / uint8, dimensions across the kernel variants, m up to 8,
+# degrees with ragged wave rounds, float32 attribute columns
+
+SHAPES = [
+    # dtype, d, m, R, f32 column
+    ("f32", 4, 1, 8, False),
+    ("f32", 32, 3, 33, True),
+    ("f32", 96, 2, 64, False),
+    ("f32", 128, 2, 64, True),
+    ("f32", 200, 4, 17, False),
+    ("f32", 768, 4, 48, True),
+    ("f32", 1024, 8, 12, True),
+    ("u8", 16, 1, 9, False),
+    ("u8", 128, 2, 32, False),
+    ("u8", 96, 5, 40, True),
+    ("u8", 1024, 2, 64, False),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=[f"{s[0]}-d{s[1]}-m{s[2]}-R{s[3]}" for s in SHAPES])
+def test_shapes(shape):
+    dtype, d, m, R, f32col = shape
+    boa = _boa()
+    arrs = random_arrays(n=3000, d=d, m=m, R=R, dtype=dtype, seed=d + m + R, f32_col=f32col)
+    orc = oracle.Index(*arrs)
+    gpu = boa.Index(*arrs)
+    q, r = random_queries(orc, 150, 40, seed=d, f32_col=f32col)
+    sched = oracle.schedule(16, 2.0, 256)
+    ref = oracle.boa(orc, q, r, 10, sched, eps=0.1)
+    got = gpu_search(gpu, q, r, k=10, L0=16, Lmax=256, eps=0.1)
+    assert_parity(got, ref, f"shape {shape}")
+    ref = oracle.boa(orc, q, r, 10, [300])
+    got = gpu_search(gpu, q, r, k=10, fixed_L=300, lds_hash_slots=2 * 64 if R < 64 else 256)
+    assert_parity(got, ref, f"shape {shape} fixed 300 with spill")
+    gpu.close()
