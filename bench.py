@@ -1,0 +1,317 @@
+#!/usr/bin/env python3
+"""Benchmark of the BOA adaptive filtered search on one MI355X.
+
+One step = one adaptive search (all phases) of the whole query batch of
+the workload, with the index, queries and ranges resident in HBM. Prints
+one JSON line: filtered QPS, recall@10 against exhaustive filtered search,
+average final beamwidth, the fixed-width (L=500) baseline built from the
+same kernel, the roofline position of the search kernel (algorithmic
+gathered bytes over the kernel's HIP-event time), and the CPU oracle timed
+on the host cores.
+
+The graph is built in-process by the workloads package (exact kNN on the
+GPU with torch matmul, then pruning and a navigation layer); that is input
+preparation, outside the timed region.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "filtered QPS at recall@10 >= 0.95 (1 GPU); avg beamwidth; HBM GB/s vs peak"
+HBM_PEAK_GBS = 8000.0
+KERNEL = "boa::phase_kernel"
+
+
+def log(msg: str):
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def exact_filtered_topk(torch, X, attrs_t, f32_cols, Q, ranges_t, k, chunk=256):
+    """Exhaustive filtered top-k on the GPU (measurement only): squared L2 by
+    the norm expansion in float64 from float32 GEMM pieces, predicates per
+    column type. Returns ids (nq,k) int64, d (nq,k) float64, n_valid (nq)."""
+    n = X.shape[0]
+    xn = (X.double() ** 2).sum(1)
+    ids_out, d_out, nv_out = [], [], []
+    a_i = attrs_t
+    a_f = attrs_t.view(torch.float32)
+    for s in range(0, Q.shape[0], chunk):
+        q = Q[s:s + chunk]
+        r = ranges_t[s:s + chunk]
+        dot = (q @ X.T).double()
+        d = (q.double() ** 2).sum(1)[:, None] + xn[None, :] - 2.0 * dot
+        valid = torch.ones((q.shape[0], n), dtype=torch.bool, device=X.device)
+        for j in range(attrs_t.shape[1]):
+            if j in f32_cols:
+                col = a_f[:, j][None, :]
+                lo = r[:, j, 0].view(torch.float32)[:, None]
+                hi = r[:, j, 1].view(torch.float32)[:, None]
+            else:
+                col = a_i[:, j][None, :]
+                lo = r[:, j, 0][:, None]
+                hi = r[:, j, 1][:, None]
+            valid &= (lo <= col) & (col <= hi)
+        d = torch.where(valid, d, torch.full_like(d, float("inf")))
+        # candidates by the expanded form, then exact float64 distances by the
+        # direct form (the expansion cancels badly for near points)
+        kk = min(n, k + 32)
+        dv, di = torch.topk(d, kk, dim=1, largest=False, sorted=True)
+        xd = X[di].double() - q.double()[:, None, :]
+        de = (xd * xd).sum(-1)
+        de = torch.where(torch.isfinite(dv), de, torch.full_like(de, float("inf")))
+        o = torch.argsort(di, dim=1, stable=True)
+        de, di = de.gather(1, o), di.gather(1, o)
+        o = torch.argsort(de, dim=1, stable=True)
+        ids_out.append(di.gather(1, o)[:, :k])
+        d_out.append(de.gather(1, o)[:, :k])
+        nv_out.append(valid.sum(1))
+        del dot, d, valid, xd
+    return torch.cat(ids_out).cpu().numpy(), torch.cat(d_out).cpu().numpy(), torch.cat(nv_out).cpu().numpy()
+
+
+def recall(ids, dists, gt_ids, gt_d, n_valid, k):
+    """strict: |found ∩ GT| / min(k, |D_f|); tie-tolerant: found valid ids
+    whose distance does not exceed the k-th exact distance (rel 1e-5)."""
+    ids = ids.astype(np.int64)
+    denom = np.maximum(1, np.minimum(k, n_valid))
+    strict = np.zeros(len(ids))
+    tie = np.zeros(len(ids))
+    for i in range(len(ids)):
+        f = ids[i][ids[i] != 0xFFFFFFFF]
+        g = gt_ids[i][np.isfinite(gt_d[i])]
+        strict[i] = len(set(f.tolist()) & set(g.tolist())) / denom[i]
+        if len(g):
+            dk = gt_d[i][len(g) - 1]
+            fd = dists[i][:len(f)].astype(np.float64)
+            tie[i] = min(k, int((fd <= dk * (1 + 1e-5) + 1e-12).sum())) / denom[i]
+        else:
+            tie[i] = 1.0 if len(f) == 0 else 0.0
+    return float(strict.mean()), float(tie.mean())
+
+
+def recorded_traffic(workload: str):
+    """HBM bytes per launch from the committed counter runs, only while the
+    kernel source is the one they measured (else None)."""
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))[workload]
+        src = os.path.join(ROOT, "paper_2609_16175_amd", "csrc", "boa_kernels.hip")
+        if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["kernel_src_sha256"]:
+            return None
+        return float(rec["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def gathered_bytes(stats) -> float:
+    return float(sum(p["gathered_bytes"] for p in stats["phases"]))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="sift-like-1M-d128")
+    ap.add_argument("--n", type=int, default=0, help="scale the workload down to n points (testing)")
+    ap.add_argument("--nq", type=int, default=0)
+    ap.add_argument("--eps", type=float, default=0.05)
+    ap.add_argument("--alpha", type=float, default=2.0)
+    ap.add_argument("--fixed-steps", type=int, default=3)
+    ap.add_argument("--no-fixed", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle timing")
+    ap.add_argument("--json-out", default="")
+    ap.add_argument("--graph-cache", default="", help="npz file: load the graph if present, else save it")
+    ap.add_argument("--copy-probe", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only: the search is query-parallel "
+                                   "and runs on a single MI355X; multi-GPU query sharding is not built",
+                          "n_gpus": args.gpus}), flush=True)
+        sys.exit(2)
+
+    import torch
+    if args.copy_probe:
+        n = args.copy_probe * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n * 4, "launches": 3}), flush=True)
+        return
+
+    import paper_2609_16175_amd as boa
+    from workloads import gen, graph
+
+    wl = gen.BY_NAME[args.workload]
+    if args.n:
+        wl = wl.scaled(args.n, nq=args.nq or None)
+    elif args.nq:
+        wl = wl.scaled(wl.n, nq=args.nq, n_clusters=wl.n_clusters)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    t = time.time()
+    data = gen.generate(wl)
+    log(f"generated {wl.name}: n={wl.n} d={wl.d} m={wl.m} nq={wl.nq} in {time.time() - t:.1f}s")
+    t = time.time()
+    if args.graph_cache and os.path.exists(args.graph_cache):
+        z = np.load(args.graph_cache)
+        adj, entry = z["adj"], int(z["entry"])
+    else:
+        adj, entry = graph.build_graph(data.vectors, wl.R, device=dev)
+        if args.graph_cache:
+            np.savez(args.graph_cache, adj=adj, entry=entry)
+    deg = float((adj != graph.PAD).sum(1).mean())
+    log(f"graph R={wl.R} (mean degree {deg:.1f}) entry={entry} in {time.time() - t:.1f}s")
+    torch.cuda.empty_cache()
+
+    types = np.array(wl.attr_dtypes, dtype=np.int32)
+    f32_cols = {j for j, tt in enumerate(wl.attr_dtypes) if tt == gen.ATTR_F32}
+    t = time.time()
+    Xg = torch.from_numpy(data.vectors).to(dev).float()
+    Qg = torch.from_numpy(data.queries).to(dev).float()
+    Ag = torch.from_numpy(data.attrs).to(dev)
+    Rg = torch.from_numpy(data.ranges).to(dev)
+    gt_ids, gt_d, n_valid = exact_filtered_topk(torch, Xg, Ag, f32_cols, Qg, Rg, wl.k)
+    del Xg, Qg, Ag
+    torch.cuda.empty_cache()
+    log(f"exhaustive filtered top-{wl.k} in {time.time() - t:.1f}s; selectivity median "
+        f"{np.median(n_valid) / wl.n:.4f}, min valid {int(n_valid.min())}")
+
+    index = boa.Index(data.vectors, data.attrs, types, adj, entry)
+    q = torch.from_numpy(data.queries).to(dev)
+    r = torch.from_numpy(data.ranges).to(dev)
+    kw = dict(k=wl.k, L0=wl.L0, Lmax=wl.Lmax, alpha=args.alpha, eps=args.eps)
+
+    for _ in range(args.warmup):
+        out = index.search(q, r, **kw)
+    index.reset_counters()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        out = index.search(q, r, **kw)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / args.steps
+    st = index.stats()
+    qps = wl.nq / (ms / 1e3)
+    log(f"adaptive: {ms:.3f} ms/step, {qps:,.0f} QPS")
+
+    ids = out.ids.cpu().numpy().view(np.uint32)
+    dists = out.dists.cpu().numpy()
+    final_L = out.final_L.cpu().numpy()
+    rec_strict, rec_tie = recall(ids, dists, gt_ids, gt_d, n_valid, wl.k)
+    sched = [p["L"] for p in st["phases"]]
+    L_avg = float(final_L.mean())
+    L_work = float(sum(p["L"] * p["active"] for p in st["phases"]) / wl.nq)
+    split = {str(p["L"]): round(100.0 * float((final_L == p["L"]).mean()), 2) for p in st["phases"]}
+    log(f"recall@10 {rec_tie:.4f} (strict {rec_strict:.4f}); L_avg {L_avg:.1f}; split {split}")
+
+    # roofline: the search kernel (every phase launch is the same kernel)
+    bytes_step = gathered_bytes(st)
+    launches_step = st["cum_launches"] / max(1, st["cum_searches"])
+    avg_launch_ms = st["cum_kernel_ms"] / max(1, st["cum_launches"])
+    bytes_launch = bytes_step / launches_step
+    achieved = bytes_launch / (avg_launch_ms * 1e-3) / 1e9
+    kernel_share = st["cum_kernel_ms"] / (ms * args.steps)
+    log(f"kernel: {avg_launch_ms:.4f} ms/launch avg over {st['cum_launches']} launches, "
+        f"{bytes_launch / 1e6:.2f} MB/launch -> {achieved:.1f} GB/s; kernel time share {kernel_share:.2f}")
+
+    fixed = None
+    if not args.no_fixed:
+        fkw = dict(k=wl.k, fixed_L=500)
+        out_f = index.search(q, r, **fkw)
+        torch.cuda.synchronize()
+        tf0 = time.perf_counter()
+        for _ in range(args.fixed_steps):
+            out_f = index.search(q, r, **fkw)
+        torch.cuda.synchronize()
+        msf = (time.perf_counter() - tf0) * 1e3 / args.fixed_steps
+        stf = index.stats()
+        rs, rt = recall(out_f.ids.cpu().numpy().view(np.uint32), out_f.dists.cpu().numpy(),
+                        gt_ids, gt_d, n_valid, wl.k)
+        fixed = dict(L=500, ms_per_step=round(msf, 4), qps=round(wl.nq / (msf / 1e3), 1),
+                     recall_at_10=round(rt, 5), recall_at_10_strict=round(rs, 5),
+                     gathered_GBps=round(gathered_bytes(stf) / (stf["phases"][0]["kernel_ms"] * 1e-3) / 1e9, 1))
+        log(f"fixed L=500: {msf:.3f} ms/step, {fixed['qps']:,.0f} QPS, recall {rt:.4f}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = min(16, os.cpu_count() or 1)
+        oix = oracle.Index(data.vectors, data.attrs, types, adj, entry)
+        osched = oracle.schedule(wl.L0, args.alpha, wl.Lmax)
+        # calibrate, then size the sample to the time budget
+        n0 = min(wl.nq, 4 * threads)
+        tc = time.perf_counter()
+        oracle.boa(oix, data.queries[:n0], data.ranges[:n0], wl.k, osched, eps=args.eps, threads=threads)
+        per_q = (time.perf_counter() - tc) / n0
+        ns = int(min(wl.nq, max(n0, args.cpu_seconds / max(per_q, 1e-6))))
+        tc = time.perf_counter()
+        ref = oracle.boa(oix, data.queries[:ns], data.ranges[:ns], wl.k, osched, eps=args.eps, threads=threads)
+        el = time.perf_counter() - tc
+        same = int(((ref.ids == ids[:ns]).all(1) & (ref.final_L == final_L[:ns])).sum())
+        cpu = dict(value=round(ns / el, 2), unit="queries/s", cores=threads, kind="oracle",
+                   sample=f"first {ns} of {wl.nq} queries, full adaptive schedule, {threads} threads, "
+                          f"{el:.1f}s wall",
+                   cpu_model=platform.processor() or platform.machine(),
+                   gpu_identical_on_sample=f"{same}/{ns}")
+        log(f"cpu oracle: {cpu['value']:.1f} QPS on {ns} queries x {threads} threads; "
+            f"GPU identical on {same}/{ns}")
+
+    res = {
+        "metric": METRIC,
+        "value": round(qps, 1),
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if wl.vec_dtype == gen.VEC_F32 else "u8",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "n": wl.n, "d": wl.d, "R": wl.R, "m": wl.m, "nq": wl.nq,
+                   "k": wl.k, "L0": wl.L0, "Lmax": wl.Lmax, "alpha": args.alpha, "eps": args.eps,
+                   "schedule": sched, "mode": "BOA"},
+        "recall_at_10": round(rec_tie, 5),
+        "recall_at_10_strict": round(rec_strict, 5),
+        "L_avg": round(L_avg, 2),
+        "L_work": round(L_work, 2),
+        "phase_split_pct": split,
+        "phases": [{k2: (round(v, 4) if isinstance(v, float) else v) for k2, v in p.items()}
+                   for p in st["phases"]],
+        "fixed_L500": fixed,
+        "speedup_vs_fixed_L500": round(qps / fixed["qps"], 3) if fixed else None,
+        "roofline": {"bound": "hbm", "kernel": KERNEL, "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": recorded_traffic(wl.name), "bytes_per_launch": round(bytes_launch),
+                     "avg_launch_ms": round(avg_launch_ms, 5), "launches": st["cum_launches"]},
+        "cpu_baseline": cpu,
+    }
+    line = json.dumps(res)
+    print(line, flush=True)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(line + "\n")
+
+
+if __name__ == "__main__":
+    main()

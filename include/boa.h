@@ -147,10 +147,19 @@ typedef struct {
     int32_t lds_hash_slots;          /* of the first phase */
     int64_t spilled_queries;         /* query-phases whose visited set left LDS */
     float total_ms;                  /* device time of the whole search */
+    /* accumulated since boa_reset_counters: searches, search-kernel launches,
+       and their summed device time (HIP events around every launch) */
+    int64_t cum_searches, cum_launches;
+    double cum_kernel_ms;
     boa_phase_stats phase[BOA_MAX_PHASES];
 } boa_stats;
 
+/* Statistics of the last search (per phase) plus the accumulated counters.
+ * Copies per-query counters back from the device: call it outside timed code. */
 int boa_get_stats(const boa_index *idx, boa_stats *out);
+
+/* Zero the accumulated counters of boa_stats. */
+int boa_reset_counters(boa_index *idx);
 
 void boa_free_index(boa_index *idx);
 

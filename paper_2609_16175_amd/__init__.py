@@ -48,6 +48,7 @@ class PhaseStats(C.Structure):
 class Stats(C.Structure):
     _fields_ = [("n_phases", C.c_int32), ("waves_per_block", C.c_int32), ("blocks", C.c_int32),
                 ("lds_hash_slots", C.c_int32), ("spilled_queries", C.c_int64), ("total_ms", C.c_float),
+                ("cum_searches", C.c_int64), ("cum_launches", C.c_int64), ("cum_kernel_ms", C.c_double),
                 ("phase", PhaseStats * MAX_PHASES)]
 
 
@@ -70,6 +71,8 @@ def lib():
         L.boa_search.argtypes = [P, P, P, C.c_int64, C.POINTER(Params), P, P, P, P, P, P]
         L.boa_get_stats.restype = C.c_int
         L.boa_get_stats.argtypes = [P, C.POINTER(Stats)]
+        L.boa_reset_counters.restype = C.c_int
+        L.boa_reset_counters.argtypes = [P]
         L.boa_free_index.restype = None
         L.boa_free_index.argtypes = [P]
         L.boa_last_error.restype = C.c_char_p
@@ -192,4 +195,8 @@ class Index:
                                gathered_bytes=ph.gathered_bytes, kernel_ms=ph.kernel_ms))
         return dict(phases=phases, waves_per_block=s.waves_per_block, blocks=s.blocks,
                     lds_hash_slots=s.lds_hash_slots, spilled_queries=s.spilled_queries,
-                    total_ms=s.total_ms)
+                    total_ms=s.total_ms, cum_searches=s.cum_searches, cum_launches=s.cum_launches,
+                    cum_kernel_ms=s.cum_kernel_ms)
+
+    def reset_counters(self):
+        _check(lib().boa_reset_counters(self._h))

@@ -111,6 +111,8 @@ struct boa_index {
     std::vector<std::pair<int, int>> launch_phase;  // (phase, event index)
     hipEvent_t ev_all0 = nullptr, ev_all1 = nullptr;
     bool have_stats = false;
+    int64_t cum_searches = 0, cum_launches = 0;
+    double cum_kernel_ms = 0.0;
 };
 
 extern "C" {
@@ -507,6 +509,13 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     ix->last_nq = nq;
     ix->last_k = p->k;
     ix->have_stats = true;
+    ix->cum_searches += 1;
+    for (auto &lp : ix->launch_phase) {
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, ix->ev_start[lp.second], ix->ev_end[lp.second]));
+        ix->cum_kernel_ms += ms;
+        ix->cum_launches += 1;
+    }
     if (status & BOA_STATUS_OVERFLOW)
         return fail(BOA_EOVERFLOW, "a visited table overflowed; results are not valid");
     return BOA_OK;
@@ -554,5 +563,17 @@ extern "C" int boa_get_stats(const boa_index *ix, boa_stats *out)
     float tot = 0.f;
     HIP_TRY(hipEventElapsedTime(&tot, ix->ev_all0, ix->ev_all1));
     out->total_ms = tot;
+    out->cum_searches = ix->cum_searches;
+    out->cum_launches = ix->cum_launches;
+    out->cum_kernel_ms = ix->cum_kernel_ms;
+    return BOA_OK;
+}
+
+extern "C" int boa_reset_counters(boa_index *ix)
+{
+    if (!ix) return fail(BOA_EINVAL, "NULL index");
+    ix->cum_searches = 0;
+    ix->cum_launches = 0;
+    ix->cum_kernel_ms = 0.0;
     return BOA_OK;
 }

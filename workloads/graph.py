@@ -26,11 +26,17 @@ search implementation.
 from __future__ import annotations
 
 import math
+import sys
+import time
 
 import numpy as np
 import torch
 
 PAD = 0xFFFFFFFF
+
+
+def _log(msg: str):
+    print(f"[graph {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
 def _as_float(x: np.ndarray, dev: torch.device) -> torch.Tensor:
@@ -166,7 +172,9 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
     Kc = min(2 * R, n - 1)
 
     # 1-2: exact kNN candidates, pruned.
+    t0 = time.time()
     du, cand = knn(X, Kc)
+    _log(f"exact {Kc}-NN of {n} points in {time.time() - t0:.1f}s")
     R_long = max(1, R // 16)
     K_nav = max(2, R // 2)
 
@@ -175,6 +183,7 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
     keep0 = alpha_prune(X, cand, du, torch.ones_like(cand, dtype=torch.bool), base_budget, alpha)
     rows0 = torch.where(keep0, cand, torch.full_like(cand, -1)).cpu().numpy()
     lab = _components(n, rows0)
+    _log(f"pruned; {lab.max() + 1} components of the kNN graph ({time.time() - t0:.1f}s)")
     first_of = np.full(lab.max() + 1, n, dtype=np.int64)
     np.minimum.at(first_of, lab, np.arange(n))
     g = np.random.Generator(np.random.PCG64(seed))
@@ -230,7 +239,7 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
     adj[for_rows >= 0] = for_rows[for_rows >= 0].astype(np.uint32)
 
     # 4: connectivity repair from the entry point.
-    print('unreachable before repair', int((~_reachable(n, adj, s_id)).sum()))
+    _log(f"assembled rows; {int((~_reachable(n, adj, s_id)).sum())} points unreachable before repair")
     adj = repair(adj, vectors, s_id, P, cand.cpu().numpy())
     return adj, s_id
 
