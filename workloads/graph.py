@@ -75,8 +75,9 @@ def _sort_by_dist_then_id(dist: torch.Tensor, ids: torch.Tensor):
 
 
 def knn(X: torch.Tensor, K: int, targets: torch.Tensor | None = None, exclude_self=True,
-        chunk: int = 4096):
-    """K nearest rows of `targets` (default X) for every row of X; (dist, ids) sorted."""
+        chunk: int = 4096, mask_fn=None):
+    """K nearest rows of `targets` (default X) for every row of X; (dist, ids) sorted.
+    mask_fn(s, e) -> bool (e-s) x T marks targets to exclude for rows s..e."""
     T = X if targets is None else targets
     nx = (X * X).sum(1)
     nt = nx if targets is None else (T * T).sum(1)
@@ -91,6 +92,8 @@ def knn(X: torch.Tensor, K: int, targets: torch.Tensor | None = None, exclude_se
         if exclude_self:
             r = torch.arange(s, e, device=X.device)
             D[r - s, r] = float("inf")
+        if mask_fn is not None:
+            D.masked_fill_(mask_fn(s, e), float("inf"))
         dv, di = torch.topk(D, kk, dim=1, largest=False, sorted=True)
         dv, di = _sort_by_dist_then_id(dv, di)
         out_d[s:e], out_i[s:e] = dv[:, :K], di[:, :K]
@@ -127,6 +130,42 @@ def alpha_prune(X: torch.Tensor, cand: torch.Tensor, du: torch.Tensor, valid: to
         keep_all[s:e] = keep
         del V, G, Dvv
     return keep_all
+
+
+def _with_reverse(cand, du, keep, width):
+    """Each row's kept candidates plus the rows that kept it (closest first),
+    deduplicated, sorted by (distance, id), cut to `width` (missing = inf)."""
+    n, K = cand.shape
+    dev = cand.device
+    src = torch.arange(n, device=dev)[:, None].expand(n, K)[keep]
+    dst = cand[keep]
+    dd = du[keep]
+    # group reverse edges by destination, nearest first, at most `width` each
+    o = torch.argsort(dd, stable=True)
+    src, dst, dd = src[o], dst[o], dd[o]
+    o = torch.argsort(dst, stable=True)
+    src, dst, dd = src[o], dst[o], dd[o]
+    start = torch.zeros(n + 1, dtype=torch.int64, device=dev)
+    start[1:] = torch.cumsum(torch.bincount(dst, minlength=n), 0)
+    rank = torch.arange(dst.numel(), device=dev) - start[dst]
+    ok = rank < width
+    rev_i = torch.full((n, width), -1, dtype=torch.int64, device=dev)
+    rev_d = torch.full((n, width), float("inf"), dtype=du.dtype, device=dev)
+    rev_i[dst[ok], rank[ok]] = src[ok]
+    rev_d[dst[ok], rank[ok]] = dd[ok]
+    fw_i = torch.where(keep, cand, torch.full_like(cand, -1))
+    fw_d = torch.where(keep, du, torch.full_like(du, float("inf")))
+    ids = torch.cat([fw_i, rev_i], 1)
+    ds = torch.cat([fw_d, rev_d], 1)
+    # dedupe: sort by id, drop repeats
+    o = torch.argsort(ids, dim=1, stable=True)
+    ids, ds = ids.gather(1, o), ds.gather(1, o)
+    rep = torch.zeros_like(ids, dtype=torch.bool)
+    rep[:, 1:] = ids[:, 1:] == ids[:, :-1]
+    ds = torch.where(rep | (ids < 0), torch.full_like(ds, float("inf")), ds)
+    ds, ids = _sort_by_dist_then_id(ds, ids.clamp_min(0))
+    ids = torch.where(torch.isfinite(ds), ids, torch.full_like(ids, -1))
+    return ids[:, :width], ds[:, :width]
 
 
 def _compact(a: torch.Tensor, width: int) -> torch.Tensor:
@@ -175,13 +214,19 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
     t0 = time.time()
     du, cand = knn(X, Kc)
     _log(f"exact {Kc}-NN of {n} points in {time.time() - t0:.1f}s")
-    R_long = max(1, R // 16)
+    R_cross = max(2, R // 4)
+    R_long = R_cross + 1
     K_nav = max(2, R // 2)
 
-    # 3: navigation sample (seeded sample + component representatives + entry).
-    base_budget = torch.full((n,), R - R_long, dtype=torch.int64, device=dev)
+    # reverse edges (NSG/Vamana style): every kept edge u->v offers u to v.
+    reserve = 1 if R >= 8 else 0   # one free slot per row for the connectivity repair
+    base_budget = torch.full((n,), R - R_long - reserve, dtype=torch.int64, device=dev)
     keep0 = alpha_prune(X, cand, du, torch.ones_like(cand, dtype=torch.bool), base_budget, alpha)
-    rows0 = torch.where(keep0, cand, torch.full_like(cand, -1)).cpu().numpy()
+    cand, du = _with_reverse(cand, du, keep0, Kc)
+    rows0 = torch.where(torch.isfinite(du), cand, torch.full_like(cand, -1)).cpu().numpy()
+    _log(f"forward-pruned + reverse candidates ({time.time() - t0:.1f}s)")
+
+    # 3: navigation sample (seeded sample + component representatives + entry).
     lab = _components(n, rows0)
     _log(f"pruned; {lab.max() + 1} components of the kNN graph ({time.time() - t0:.1f}s)")
     first_of = np.full(lab.max() + 1, n, dtype=np.int64)
@@ -200,6 +245,7 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
     KP = min(len(P) - 1, 256)
     dPP, iPP = knn(XP, KP)
     labP = torch.from_numpy(lab[P]).to(dev)
+    lab_t = torch.from_numpy(lab).to(dev)
     other = labP[iPP] != labP[:, None]
     nav_keep = alpha_prune(XP, iPP, dPP, other,
                            torch.full((len(P),), K_nav, dtype=torch.int64, device=dev), alpha)
@@ -207,11 +253,22 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
     nav_links = torch.full((n, K_nav), -1, dtype=torch.int64, device=dev)
     nav_links[Pt] = nav_ids
 
-    # every point: its nearest sample points other than itself.
-    _, iNear = knn(X, R_long + 1, targets=XP, exclude_self=False)
-    near = Pt[iNear]
-    near = _compact(torch.where(near == torch.arange(n, device=dev)[:, None],
-                                torch.full_like(near, -1), near), R_long)
+    # every point: links to nearby components (alpha-pruned over its nearest
+    # sample points of other components) and to its own component's nearest
+    # sample point, so that every expansion also looks across components.
+    Kx = min(len(P), 4 * R_cross)
+    d_near, i_near = knn(X, Kx, targets=XP, exclude_self=False,
+                         mask_fn=lambda s, e: labP[None, :] == lab_t[s:e, None])
+    cross_keep = alpha_prune(XP, i_near, d_near, torch.isfinite(d_near),
+                             torch.full((n,), R_cross, dtype=torch.int64, device=dev), alpha)
+    cross = _compact(torch.where(cross_keep, Pt[i_near], torch.full_like(i_near, -1)), R_cross)
+    d_own, i_own = knn(X, min(2, len(P)), targets=XP, exclude_self=False,
+                       mask_fn=lambda s, e: labP[None, :] != lab_t[s:e, None])
+    own = Pt[i_own]
+    bad = (own == torch.arange(n, device=dev)[:, None]) | ~torch.isfinite(d_own)
+    own = _compact(torch.where(bad, torch.full_like(own, -1), own), 1)
+    near = torch.cat([cross, own], 1)
+    _log(f"navigation: {len(P)} sample points, {R_cross} cross-component links per point")
 
     long = torch.cat([nav_links, near], 1)
     dup = torch.zeros_like(long, dtype=torch.bool)
@@ -224,7 +281,7 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
     in_long = torch.zeros_like(cand, dtype=torch.bool)
     for j in range(long.shape[1]):
         in_long |= cand == long[:, j:j + 1]
-    keep = alpha_prune(X, cand, du, ~in_long, R - n_long, alpha)
+    keep = alpha_prune(X, cand, du, ~in_long & torch.isfinite(du), R - n_long - reserve, alpha)
 
     adj = np.full((n, R), PAD, dtype=np.uint32)
     longn = long.cpu().numpy()
@@ -245,51 +302,66 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
 
 
 def repair(adj: np.ndarray, vectors: np.ndarray, s_id: int, P: np.ndarray,
-           cand: np.ndarray, rounds: int = 8):
+           cand: np.ndarray, rounds: int = 32):
     """Make every point reachable from s_id.
 
-    An unreachable point v gets an in-edge from the nearest reachable point
-    among its own kNN candidates (else the nearest reachable sample point):
-    into a padding slot if the row has one, else replacing the row's
-    farthest out-edge whose target keeps another in-edge.
+    An unreachable point v gets an in-edge from a reachable point w: the
+    nearest reachable point among v's own candidates, else among the 64
+    sample points nearest v. The edge goes into a free slot of w's row when
+    there is one, else replaces w's farthest out-edge whose target has at
+    least two in-edges from reachable points (so it stays reachable).
     """
     n, R = adj.shape
-    indeg = np.bincount(adj[adj != PAD].astype(np.int64), minlength=n)
+
+    def reach_indeg(seen):
+        src = np.repeat(seen, R)
+        t = adj.reshape(-1).astype(np.int64)
+        ok = src & (adj.reshape(-1) != PAD)
+        return np.bincount(t[ok], minlength=n)
+
     for _ in range(rounds):
         seen = _reachable(n, adj, s_id)
         if seen.all():
             return adj
+        indeg = reach_indeg(seen)
         ok_P = P[seen[P]]
         ok_Pf = vectors[ok_P].astype(np.float64)
         for v in np.flatnonzero(~seen):
             if seen[v]:
                 continue
-            ws = [int(w) for w in cand[v] if w >= 0 and seen[w]]
-            if not ws:
-                x = vectors[v].astype(np.float64)
-                ws = [int(ok_P[i]) for i in np.argsort(((ok_Pf - x) ** 2).sum(1), kind="stable")[:64]]
+            ws = [int(w) for w in cand[v] if w >= 0 and seen[w] and w != v]
+            x = vectors[v].astype(np.float64)
+            ws += [int(ok_P[i]) for i in np.argsort(((ok_Pf - x) ** 2).sum(1), kind="stable")[:64]
+                   if ok_P[i] != v]
+            linked = False
             for w in ws:
-                if w == v:
-                    continue
                 row = adj[w]
                 pads = np.flatnonzero(row == PAD)
                 if pads.size:
-                    slot = int(pads[0])
-                else:
+                    row[pads[0]] = v
+                    linked = True
+                    break
+            if not linked:
+                for w in ws:
+                    row = adj[w]
                     movable = [j for j in range(R - 1, -1, -1) if indeg[row[j]] >= 2]
-                    if not movable:
-                        continue
-                    slot = movable[0]
-                    indeg[row[slot]] -= 1
-                row[slot] = v
-                indeg[v] += 1
-                break
+                    if movable:
+                        indeg[row[movable[0]]] -= 1
+                        row[movable[0]] = v
+                        linked = True
+                        break
+            if not linked:
+                continue
+            indeg[v] += 1
             stack = [v]
             seen[v] = True
             while stack:
                 u = stack.pop()
                 for t in adj[u]:
-                    if t != PAD and not seen[t]:
+                    if t == PAD:
+                        continue
+                    indeg[t] += 1
+                    if not seen[t]:
                         seen[t] = True
                         stack.append(int(t))
     seen = _reachable(n, adj, s_id)
