@@ -199,23 +199,35 @@ def main():
     r = torch.from_numpy(data.ranges).to(dev)
     kw = dict(k=wl.k, L0=wl.L0, Lmax=wl.Lmax, alpha=args.alpha, eps=args.eps)
 
-    for _ in range(args.warmup):
-        out = index.search(q, r, **kw)
-    index.reset_counters()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        out = index.search(q, r, **kw)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms = (t1 - t0) * 1e3 / args.steps
-    st = index.stats()
+    def timed(search_kw, steps, warmup):
+        """warm-up, then `steps` timed searches bracketed by device syncs;
+        per-launch kernel time comes from the library's HIP events."""
+        o = None
+        for _ in range(warmup):
+            o = index.search(q, r, **search_kw)
+        index.reset_counters()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            o = index.search(q, r, **search_kw)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        return (t1 - t0) * 1e3 / steps, index.stats(), o
+
+    modes = {}
+    for mode in ("phased", "fused"):
+        ms_m, st_m, out_m = timed(dict(kw, fused=(mode == "fused")), args.steps, args.warmup)
+        modes[mode] = (ms_m, st_m, out_m)
+        log(f"adaptive ({mode}): {ms_m:.3f} ms/step, {wl.nq / (ms_m / 1e3):,.0f} QPS")
+    mode = min(modes, key=lambda k2: modes[k2][0])
+    ms, st, out = modes[mode]
     qps = wl.nq / (ms / 1e3)
-    log(f"adaptive: {ms:.3f} ms/step, {qps:,.0f} QPS")
 
     ids = out.ids.cpu().numpy().view(np.uint32)
     dists = out.dists.cpu().numpy()
     final_L = out.final_L.cpu().numpy()
+    for m2, (_, _, o2) in modes.items():
+        assert np.array_equal(o2.ids.cpu().numpy().view(np.uint32), ids), f"{m2} results differ"
     rec_strict, rec_tie = recall(ids, dists, gt_ids, gt_d, n_valid, wl.k)
     sched = [p["L"] for p in st["phases"]]
     L_avg = float(final_L.mean())
@@ -223,27 +235,19 @@ def main():
     split = {str(p["L"]): round(100.0 * float((final_L == p["L"]).mean()), 2) for p in st["phases"]}
     log(f"recall@10 {rec_tie:.4f} (strict {rec_strict:.4f}); L_avg {L_avg:.1f}; split {split}")
 
-    # roofline: the search kernel (every phase launch is the same kernel)
+    # roofline: the search kernel (every launch is the same kernel)
     bytes_step = gathered_bytes(st)
     launches_step = st["cum_launches"] / max(1, st["cum_searches"])
     avg_launch_ms = st["cum_kernel_ms"] / max(1, st["cum_launches"])
     bytes_launch = bytes_step / launches_step
     achieved = bytes_launch / (avg_launch_ms * 1e-3) / 1e9
     kernel_share = st["cum_kernel_ms"] / (ms * args.steps)
-    log(f"kernel: {avg_launch_ms:.4f} ms/launch avg over {st['cum_launches']} launches, "
+    log(f"kernel ({mode}): {avg_launch_ms:.4f} ms/launch avg over {st['cum_launches']} launches, "
         f"{bytes_launch / 1e6:.2f} MB/launch -> {achieved:.1f} GB/s; kernel time share {kernel_share:.2f}")
 
     fixed = None
     if not args.no_fixed:
-        fkw = dict(k=wl.k, fixed_L=500)
-        out_f = index.search(q, r, **fkw)
-        torch.cuda.synchronize()
-        tf0 = time.perf_counter()
-        for _ in range(args.fixed_steps):
-            out_f = index.search(q, r, **fkw)
-        torch.cuda.synchronize()
-        msf = (time.perf_counter() - tf0) * 1e3 / args.fixed_steps
-        stf = index.stats()
+        msf, stf, out_f = timed(dict(k=wl.k, fixed_L=500), args.fixed_steps, 1)
         rs, rt = recall(out_f.ids.cpu().numpy().view(np.uint32), out_f.dists.cpu().numpy(),
                         gt_ids, gt_d, n_valid, wl.k)
         fixed = dict(L=500, ms_per_step=round(msf, 4), qps=round(wl.nq / (msf / 1e3), 1),
@@ -290,7 +294,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "n": wl.n, "d": wl.d, "R": wl.R, "m": wl.m, "nq": wl.nq,
                    "k": wl.k, "L0": wl.L0, "Lmax": wl.Lmax, "alpha": args.alpha, "eps": args.eps,
-                   "schedule": sched, "mode": "BOA"},
+                   "schedule": sched, "mode": f"BOA ({mode} phases)"},
+        "modes": {m2: {"ms_per_step": round(v[0], 4), "qps": round(wl.nq / (v[0] / 1e3), 1),
+                       "launches_per_step": round(v[1]["cum_launches"] / max(1, v[1]["cum_searches"]), 2)}
+                  for m2, v in modes.items()},
         "recall_at_10": round(rec_tie, 5),
         "recall_at_10_strict": round(rec_strict, 5),
         "L_avg": round(L_avg, 2),
@@ -300,9 +307,9 @@ def main():
                    for p in st["phases"]],
         "fixed_L500": fixed,
         "speedup_vs_fixed_L500": round(qps / fixed["qps"], 3) if fixed else None,
-        "roofline": {"bound": "hbm", "kernel": KERNEL, "achieved": round(achieved, 1),
+        "roofline": {"bound": "hbm", "kernel": KERNEL, "mode": mode, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": recorded_traffic(wl.name), "bytes_per_launch": round(bytes_launch),
+                     "traffic": recorded_traffic(f"{wl.name}/{mode}"), "bytes_per_launch": round(bytes_launch),
                      "avg_launch_ms": round(avg_launch_ms, 5), "launches": st["cum_launches"]},
         "cpu_baseline": cpu,
     }

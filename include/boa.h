@@ -104,6 +104,11 @@ typedef struct {
     const int32_t *schedule; /* optional host array of explicit phase widths
                                 (strictly increasing); overrides L0/Lmax/alpha */
     int32_t n_schedule;
+    int32_t fused;          /* 1: run every phase in one persistent launch, each wave
+                               carrying its query from width to width without waiting
+                               for the other queries (identical results, since every
+                               phase restarts the search; needs tau == 0). 0: one launch
+                               per phase with device-side compaction between them. */
 } boa_params;
 
 void boa_default_params(boa_params *p);

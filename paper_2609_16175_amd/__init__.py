@@ -16,7 +16,9 @@ from dataclasses import dataclass
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libboa.so")
+# BOA_LIB selects another build of the same library (e.g. the stage-profiling
+# variant libboa_stageprof.so); default: the product build.
+LIB_PATH = os.path.join(_HERE, os.environ.get("BOA_LIB", "libboa.so"))
 
 VEC_F32, VEC_U8 = 0, 1
 ATTR_I32, ATTR_F32 = 0, 1
@@ -36,7 +38,7 @@ class Params(C.Structure):
     _fields_ = [("k", C.c_int32), ("L0", C.c_int32), ("Lmax", C.c_int32), ("alpha", C.c_double),
                 ("eps", C.c_double), ("tau", C.c_double), ("fixed_L", C.c_int32),
                 ("boa_plus", C.c_int32), ("sub_batches", C.c_int32), ("lds_hash_slots", C.c_int32),
-                ("schedule", C.POINTER(C.c_int32)), ("n_schedule", C.c_int32)]
+                ("schedule", C.POINTER(C.c_int32)), ("n_schedule", C.c_int32), ("fused", C.c_int32)]
 
 
 class PhaseStats(C.Structure):
@@ -142,7 +144,8 @@ class Index:
 
     def search(self, queries, ranges, k: int, L0: int = 16, Lmax: int = 512, alpha: float = 2.0,
                eps: float = 0.05, tau: float = 0.0, fixed_L: int = 0, boa_plus: bool = False,
-               sub_batches: int = 10, lds_hash_slots: int = 0, schedule=None, counters: bool = False,
+               sub_batches: int = 10, lds_hash_slots: int = 0, schedule=None, fused: bool = False,
+               counters: bool = False,
                stream=None, out=None) -> SearchResult:
         """Adaptive filtered top-k of a batch of device-resident queries.
 
@@ -172,6 +175,7 @@ class Index:
         p = default_params()
         p.k, p.L0, p.Lmax, p.alpha, p.eps, p.tau = k, L0, Lmax, alpha, eps, tau
         p.fixed_L, p.boa_plus, p.sub_batches, p.lds_hash_slots = fixed_L, int(boa_plus), sub_batches, lds_hash_slots
+        p.fused = int(fused)
         sched_arr = None
         if schedule is not None:
             sched_arr = (C.c_int32 * len(schedule))(*schedule)

@@ -19,16 +19,19 @@ HIPCC_FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + f".tmp{os.getpid()}"
-    cmd = ["hipcc", *HIPCC_FLAGS, *SOURCES, "-o", tmp]
+def build(verbose: bool = False, stage_profile: bool = False) -> str:
+    """Compile libboa.so; stage_profile=True builds libboa_stageprof.so, a
+    variant that prints per-stage cycle counts of every phase to stderr."""
+    lib = LIB if not stage_profile else os.path.join(PKG, "libboa_stageprof.so")
+    tmp = lib + f".tmp{os.getpid()}"
+    cmd = ["hipcc", *HIPCC_FLAGS, *(["-DBOA_STAGE_PROFILE"] if stage_profile else []), *SOURCES, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + r.stdout + r.stderr)
     if verbose:
         print(r.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":

@@ -96,10 +96,9 @@ struct boa_index {
     uint8_t *qstat = nullptr;        // ph_cap x nq
     uint32_t *qE = nullptr, *qS = nullptr;  // ph_cap x nq
     uint32_t *status = nullptr;
-    uint32_t *gtab = nullptr;
-    uint32_t *epochs = nullptr;
+    uint32_t *bits = nullptr;        // visited spill bitmaps, bits_words per wave slot
+    uint32_t bits_words = 0;
     uint64_t slots_cap = 0;
-    int32_t g_log2_cap = 0;
     uint32_t *pool = nullptr;        // BOA+ survivor pools (ph_cap x nq)
     hipStream_t aux = nullptr;       // BOA+ second stream
     std::vector<hipEvent_t> ev_start, ev_end;  // per launch
@@ -135,6 +134,7 @@ void boa_default_params(boa_params *p)
     p->lds_hash_slots = 0;
     p->schedule = nullptr;
     p->n_schedule = 0;
+    p->fused = 0;
 }
 
 void boa_free_index(boa_index *ix)
@@ -155,8 +155,7 @@ void boa_free_index(boa_index *ix)
     dfree(ix->qE);
     dfree(ix->qS);
     dfree(ix->status);
-    dfree(ix->gtab);
-    dfree(ix->epochs);
+    dfree(ix->bits);
     dfree(ix->pool);
     for (auto e : ix->ev_start) (void)hipEventDestroy(e);
     for (auto e : ix->ev_end) (void)hipEventDestroy(e);
@@ -271,8 +270,7 @@ int ensure_events(boa_index *ix, size_t count)
     return BOA_OK;
 }
 
-int ensure_workspace(boa_index *ix, int64_t nq, int32_t n_phases, uint64_t slots, int32_t g_log2,
-                     int32_t n_counters, bool plus)
+int ensure_workspace(boa_index *ix, int64_t nq, int32_t n_phases, uint64_t slots, int32_t n_counters, bool plus)
 {
     int rc;
     if (nq > ix->nq_cap || n_phases > ix->ph_cap) {
@@ -305,20 +303,18 @@ int ensure_workspace(boa_index *ix, int64_t nq, int32_t n_phases, uint64_t slots
         if ((rc = dalloc(&ix->counters, n_counters))) return rc;
         ix->n_counters = n_counters;
     }
-    if (slots > ix->slots_cap || g_log2 > ix->g_log2_cap) {
+    if (slots > ix->slots_cap) {
+        // one bit per point per wave slot, in whole 16-byte units; a query
+        // zeroes its slot's bitmap when it first spills, so no clearing here
         uint64_t sc = std::max<uint64_t>(slots, ix->slots_cap);
-        int32_t gl = std::max<int32_t>(g_log2, ix->g_log2_cap);
-        dfree(ix->gtab);
-        dfree(ix->epochs);
-        if ((rc = dalloc(&ix->gtab, (size_t)sc << gl)) || (rc = dalloc(&ix->epochs, sc))) {
+        uint32_t words = (uint32_t)(((ix->view.n + 127) / 128) * 4);
+        dfree(ix->bits);
+        if ((rc = dalloc(&ix->bits, (size_t)sc * words))) {
             ix->slots_cap = 0;
-            ix->g_log2_cap = 0;
             return rc;
         }
-        HIP_TRY(hipMemset(ix->gtab, 0, ((size_t)sc << gl) * sizeof(uint32_t)));
-        HIP_TRY(hipMemset(ix->epochs, 0, sc * sizeof(uint32_t)));
         ix->slots_cap = sc;
-        ix->g_log2_cap = gl;
+        ix->bits_words = words;
     }
     if (plus && !ix->aux) HIP_TRY(hipStreamCreateWithFlags(&ix->aux, hipStreamNonBlocking));
     return BOA_OK;
@@ -359,18 +355,28 @@ PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t m
 {
     PhasePlan pl{};
     pl.L = L;
-    uint32_t h = forced_h > 0 ? (uint32_t)forced_h
-                              : std::min<uint32_t>(8192u, std::max<uint32_t>(2048u, next_pow2(32ull * L)));
+    // visited table: 2048 slots (8 KB) at every width. The wide phases hold
+    // few queries, so a small table keeps them all resident at once; what
+    // does not fit spills to the HBM bitmap.
+    uint32_t h = forced_h > 0 ? (uint32_t)forced_h : 2048u;
     pl.h_slots = (int32_t)h;
-    pl.lds_per_wave = (int32_t)(8 * L + 64 * (8 + 4 + 4 + 4) + 4 * h);
+    const int32_t Lb = (L + 1) & ~1, pw = ((L >> 6) + 3) & ~1;
+    pl.lds_per_wave = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + 4 * (int32_t)h;
     pl.lds_per_wave = (pl.lds_per_wave + 15) & ~15;
-    int wpb = 4;
-    while (wpb > 1 && (size_t)wpb * pl.lds_per_wave > ix->lds_per_block_max) wpb >>= 1;
-    pl.wpb = wpb;
-    int occ = phase_occupancy(ix->vec_dtype, ix->view.d, wpb, (size_t)wpb * pl.lds_per_wave);
-    if (occ < 1) occ = 1;
-    int64_t blocks = (int64_t)occ * ix->num_cu;
-    int64_t need = (max_active + wpb - 1) / wpb;
+    // waves per block: the choice with the most resident waves per CU
+    int best_w = 0, best_wpb = 1, best_occ = 1;
+    for (int wpb = 4; wpb >= 1; wpb >>= 1) {
+        if ((size_t)wpb * pl.lds_per_wave > ix->lds_per_block_max) continue;
+        int occ = phase_occupancy(ix->vec_dtype, ix->view.d, wpb, (size_t)wpb * pl.lds_per_wave);
+        if (occ * wpb > best_w) {
+            best_w = occ * wpb;
+            best_wpb = wpb;
+            best_occ = occ;
+        }
+    }
+    pl.wpb = best_wpb;
+    int64_t blocks = (int64_t)std::max(best_occ, 1) * ix->num_cu;
+    int64_t need = (max_active + best_wpb - 1) / best_wpb;
     if (need < 1) need = 1;
     pl.blocks = (int32_t)std::min<int64_t>(blocks, need);
     pl.launches = 0;
@@ -401,6 +407,10 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     if (p->lds_hash_slots && (uint32_t)p->lds_hash_slots / 2 < (uint32_t)ix->view.R + 1)
         return fail(BOA_EINVAL, "lds_hash_slots too small for the graph degree");
     const bool plus = p->boa_plus != 0 && p->fixed_L <= 0;
+    const bool fused = p->fused != 0;
+    if (fused && p->tau != 0.0)
+        return fail(BOA_EINVAL, "fused phases need tau == 0 (the residual test counts all queries of a phase)");
+    if (fused && plus) return fail(BOA_EINVAL, "fused and boa_plus are exclusive");
     if (plus && (p->sub_batches < 1 || p->sub_batches > 1024)) return fail(BOA_EINVAL, "sub_batches out of range");
     if (nq == 0) return BOA_OK;
 
@@ -413,17 +423,17 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     std::vector<PhasePlan> plans;
     uint64_t slots = 0;
     for (int32_t ph = 0; ph < n_phases; ++ph) {
-        PhasePlan pl = plan_phase(ix, sched[ph], p->lds_hash_slots, nq);
+        // a fused launch sizes its LDS for the widest phase
+        PhasePlan pl = plan_phase(ix, fused ? sched.back() : sched[ph], p->lds_hash_slots, nq);
+        pl.L = sched[ph];
         if ((size_t)pl.lds_per_wave > ix->lds_per_block_max)
             return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
         slots = std::max<uint64_t>(slots, (uint64_t)pl.blocks * pl.wpb);
         plans.push_back(pl);
     }
-    const int32_t Lmax = sched.back();
-    int32_t g_log2 = ilog2(std::min<uint32_t>(1u << 20, std::max<uint32_t>(1u << 14, next_pow2(64ull * Lmax))));
     const int32_t sub = plus ? std::min<int32_t>(p->sub_batches, (int32_t)nq) : 1;
     const int32_t n_counters = n_phases * (sub + 1) + 8;
-    if ((rc = ensure_workspace(ix, nq, n_phases, plus ? 2 * slots : slots, g_log2, n_counters, plus))) return rc;
+    if ((rc = ensure_workspace(ix, nq, n_phases, plus ? 2 * slots : slots, n_counters, plus))) return rc;
     if ((rc = ensure_events(ix, (size_t)n_phases * (sub + 1)))) return rc;
     const uint32_t tau_count = (uint32_t)std::floor(p->tau * (double)nq);
 
@@ -453,17 +463,42 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     base.final_L = final_L;
     base.user_E = expansions;
     base.user_S = scored;
-    base.gtab = ix->gtab;
-    base.epochs = ix->epochs;
+    base.bits = ix->bits;
+    base.bits_words = ix->bits_words;
     base.status = ix->status;
     base.eps = p->eps;
     base.tau_count = tau_count;
     base.k = p->k;
-    base.g_log2 = ix->g_log2_cap;
     base.conf = ix->conf;
+    base.nq = nq;
+    base.qstat = ix->qstat;
+    base.qE = ix->qE;
+    base.qS = ix->qS;
+    for (int32_t ph = 0; ph < n_phases; ++ph) base.sched[ph] = sched[ph];
     int ev = 0;
 
-    if (!plus) {
+    if (fused) {
+        PhasePlan &pl = plans[0];
+        PhaseArgs a = base;
+        a.active = ix->active[0];
+        a.n_active = ix->n_active;
+        a.t_begin = 0;
+        a.t_end = 0xFFFFFFFFu;
+        a.queue = ix->counters;
+        a.p_begin = 0;
+        a.p_end = n_phases;
+        a.L_alloc = sched.back();
+        a.h_log2 = ilog2((uint32_t)pl.h_slots);
+        a.lds_per_wave = pl.lds_per_wave;
+        a.waves_per_block = pl.wpb;
+        a.slot_base = 0;
+        HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
+        HIP_TRY(launch_phase(a, ix->vec_dtype, pl.blocks, st));
+        HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
+        ix->launch_phase.push_back({0, ev});
+        ++ev;
+        pl.launches = 1;
+    } else if (!plus) {
         for (int32_t ph = 0; ph < n_phases; ++ph) {
             PhasePlan &pl = plans[ph];
             PhaseArgs a = base;
@@ -472,17 +507,40 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
             a.t_begin = 0;
             a.t_end = 0xFFFFFFFFu;
             a.queue = ix->counters + ph;
-            a.qstat = ix->qstat + (size_t)ph * nq;
-            a.qE = ix->qE + (size_t)ph * nq;
-            a.qS = ix->qS + (size_t)ph * nq;
-            a.L = pl.L;
+            a.p_begin = ph;
+            a.p_end = ph + 1;
+            a.L_alloc = pl.L;
             a.h_log2 = ilog2((uint32_t)pl.h_slots);
             a.lds_per_wave = pl.lds_per_wave;
             a.waves_per_block = pl.wpb;
             a.slot_base = 0;
+#ifdef BOA_STAGE_PROFILE
+            unsigned long long *prof = nullptr;
+            const size_t pn = (size_t)pl.blocks * pl.wpb * BOA_PROF_SLOTS;
+            HIP_TRY(hipMalloc(reinterpret_cast<void **>(&prof), pn * 8));
+            HIP_TRY(hipMemsetAsync(prof, 0, pn * 8, st));
+            a.prof = prof;
+#endif
             HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
             HIP_TRY(launch_phase(a, ix->vec_dtype, pl.blocks, st));
             HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
+#ifdef BOA_STAGE_PROFILE
+            {
+                std::vector<unsigned long long> h(pn);
+                HIP_TRY(hipMemcpyAsync(h.data(), prof, pn * 8, hipMemcpyDeviceToHost, st));
+                HIP_TRY(hipStreamSynchronize(st));
+                double tot[BOA_PROF_SLOTS] = {0};
+                for (size_t i = 0; i < pn; ++i) tot[i % BOA_PROF_SLOTS] += (double)h[i];
+                const double ne = tot[10] > 0 ? tot[10] : 1;
+                std::fprintf(stderr,
+                             "[stage-profile] L=%d waves=%d expansions=%.0f cycles/expansion: select %.0f "
+                             "visit %.0f score %.0f sort %.0f rank %.0f rebuild %.0f | spilled %.2f chunks %.2f "
+                             "row-prefetch hit %.2f reissued %.2f\n",
+                             pl.L, pl.blocks * pl.wpb, tot[10], tot[0] / ne, tot[1] / ne, tot[2] / ne, tot[3] / ne,
+                             tot[4] / ne, tot[5] / ne, tot[6] / ne, tot[7] / ne, tot[8] / ne, tot[9] / ne);
+                (void)hipFree(prof);
+            }
+#endif
             ix->launch_phase.push_back({ph, ev});
             ++ev;
             pl.launches = 1;

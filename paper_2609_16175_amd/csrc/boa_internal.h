@@ -8,6 +8,7 @@
 
 #define BOA_PAD 0xFFFFFFFFu
 #define BOA_STATUS_OVERFLOW 1u
+#define BOA_PROF_SLOTS 12
 
 namespace boa {
 
@@ -35,18 +36,23 @@ struct PhaseArgs {
     uint32_t *ids;
     float *dists;
     int32_t *final_L;
-    uint8_t *qstat;           // per query, this phase: 0 not run, 1 ran, 2 ran+confident, +4 spilled
-    uint32_t *qE, *qS;        // per query, this phase: expansions, scored
+    uint8_t *qstat;           // [phase][query]: 0 not run, 1 ran, 2 ran+confident, +4 spilled
+    uint32_t *qE, *qS;        // [phase][query]: expansions, scored
+    int64_t nq;               // stride of the per-phase arrays
     uint32_t *user_E, *user_S;// optional per-query totals over phases
-    uint32_t *gtab;           // visited spill tables, (1 << g_log2) entries per wave slot
-    uint32_t *epochs;         // per wave slot
+    uint32_t *bits;           // visited spill bitmaps, bits_words u32 per wave slot
+    uint32_t bits_words;
     uint32_t *status;
     double eps;
     uint32_t tau_count;       // the phase runs only if n_active > tau_count
-    int32_t L, k;
-    int32_t h_log2, g_log2;
+    int32_t k;
+    int32_t sched[BOA_MAX_PHASES]; // phase widths
+    int32_t p_begin, p_end;   // phases run by this launch (one, or all when fused)
+    int32_t L_alloc;          // widest of them: sizes the per-wave LDS
+    int32_t h_log2;
     int32_t lds_per_wave, waves_per_block;
     uint32_t slot_base;
+    unsigned long long *prof; // per wave slot: BOA_PROF_SLOTS stage counters (profiling builds)
 };
 
 struct CompactArgs {

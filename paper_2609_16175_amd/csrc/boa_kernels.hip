@@ -6,16 +6,20 @@
 //   1. select the first not-yet-expanded worklist entry (ballot scan);
 //   2. gather its adjacency row, one neighbour per lane (one coalesced load);
 //   3. test-and-insert every neighbour into the query's visited set: an
-//      open-addressing table in LDS that spills into a per-wave table in
-//      HBM once its load passes one half;
+//      open-addressing table in LDS that spills, once its load passes one
+//      half, into a per-wave bitmap over all points in HBM (one atomic OR
+//      per neighbour);
 //   4. for the unseen neighbours: gather the attribute cells and count the
 //      violated range predicates (phi, Eq. 2), gather the vector and compute
 //      the squared L2 distance with a 16-lane (float32) or G-lane (uint8)
 //      group per candidate and a butterfly reduction;
 //   5. pack (phi, distance, id) into one 64-bit key, drop keys that cannot
-//      enter the worklist, bitonic-sort the rest across the wave and merge
-//      them into the sorted worklist held in LDS (binary-search ranks,
-//      suffix shifted backwards in 64-entry chunks).
+//      enter the worklist, compact and bitonic-sort the rest over the
+//      smallest power-of-two lane count, and merge them into the sorted
+//      worklist held in LDS: each new key's rank by binary search, its
+//      output slot marked in a bitmap, and the suffix rebuilt backwards in
+//      64-entry chunks where a popcount of the bitmap tells every output
+//      slot where its entry comes from.
 // The epilogue writes the first k filter-valid entries, the phase width,
 // and the Eq. 3 confidence flag.
 //
@@ -30,6 +34,17 @@
 #include "boa_internal.h"
 
 namespace boa {
+
+// Optional per-stage cycle accounting (build with -DBOA_STAGE_PROFILE): each
+// wave adds the shader-clock cycles of every stage of every expansion to its
+// slot's row of PhaseArgs::prof. Off in the product build.
+#ifdef BOA_STAGE_PROFILE
+#define PROF_T(var) const uint64_t var = __builtin_amdgcn_s_memtime()
+#define PROF_ADD(i, v) (prof_acc[(i)] += (v))
+#else
+#define PROF_T(var)
+#define PROF_ADD(i, v)
+#endif
 
 static constexpr uint64_t KEY_NONE = ~0ull;
 static constexpr uint64_t KEY_PHI1 = 1ull << 60;  // smallest key with phi >= 1
@@ -90,14 +105,16 @@ __device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int m)
     return ((uint64_t)hi << 32) | lo;
 }
 
-// Ascending bitonic sort of one 64-bit key per lane across the wave.
-__device__ __forceinline__ uint64_t wave_sort64(uint64_t key, int lane)
+// Ascending bitonic sort of one 64-bit key per lane over lanes [0, W), W a
+// power of two <= 64 (lanes >= W run the same network on their own blocks).
+__device__ __forceinline__ uint64_t wave_sort64(uint64_t key, int lane, uint32_t W)
 {
 #pragma unroll
-    for (int k = 2; k <= 64; k <<= 1) {
+    for (uint32_t k = 2; k <= 64; k <<= 1) {
+        if (k > W) break;
 #pragma unroll
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            uint64_t o = shfl_xor64(key, j);
+        for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+            uint64_t o = shfl_xor64(key, (int)j);
             bool up = (lane & k) == 0;
             bool lower = (lane & j) == 0;
             uint64_t mn = key < o ? key : o;
@@ -229,17 +246,16 @@ struct U8Scorer {
 };
 
 // ---------------------------------------------------------------------------
-// Visited set. LDS table: 0 = empty, else id + 1. Global table (per wave
-// slot, in HBM): entry = epoch << 24 | id; entries of another epoch are
-// free. A wave bumps its epoch for every query that used the table and
-// clears the table when the 8-bit epoch wraps.
+// Visited set. LDS table: open addressing with linear probing, 0 = empty,
+// else id + 1. Once half full, new ids go to the wave slot's bitmap over
+// all points in HBM (one bit per point), zeroed when a query first spills;
+// every probe then checks the LDS table first and the bitmap second.
 
 struct Visited {
     uint32_t *lds;
     uint32_t lmask, lshift;
-    uint32_t *gt;
-    uint32_t gmask, gshift;
-    uint32_t epoch;
+    uint32_t *bits;      // this wave slot's bitmap, words32 words
+    uint32_t words32;
     uint32_t *status;
 };
 
@@ -275,27 +291,20 @@ __device__ __forceinline__ bool in_lds(const Visited &s, uint32_t v)
     return false;
 }
 
-__device__ __forceinline__ bool visit_global(const Visited &s, uint32_t v)
+__device__ __forceinline__ bool visit_bits(const Visited &s, uint32_t v)
 {
-    uint32_t tag = (s.epoch << 24) | v;
-    uint32_t h = (hash32(v) >> s.gshift);
-    uint32_t probe = 0;
-    uint32_t cur = s.gt[h];
-    while (probe <= s.gmask) {
-        if (cur == tag) return false;
-        if ((cur >> 24) != s.epoch) {
-            uint32_t old = atomicCAS(&s.gt[h], cur, tag);
-            if (old == cur) return true;
-            if (old == tag) return false;
-            cur = old;          // slot changed under us: look at it again
-            continue;
-        }
-        h = (h + 1u) & s.gmask;
-        ++probe;
-        cur = s.gt[h];
-    }
-    atomicOr(s.status, BOA_STATUS_OVERFLOW);
-    return false;
+    uint32_t bit = 1u << (v & 31u);
+    uint32_t old = atomicOr(&s.bits[v >> 5], bit);
+    return (old & bit) == 0u;
+}
+
+__device__ __forceinline__ void clear_bits(const Visited &s, int lane)
+{
+    uint4 z = make_uint4(0, 0, 0, 0);
+    uint4 *b4 = reinterpret_cast<uint4 *>(s.bits);
+    for (uint32_t i = lane; i < (s.words32 >> 2); i += 64) b4[i] = z;
+    // the stores must land before this wave's atomics on the same words
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
 }
 
 // ---------------------------------------------------------------------------
@@ -308,35 +317,39 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     const int wid = threadIdx.x >> 6;
     const uint32_t slot = a.slot_base + blockIdx.x * a.waves_per_block + wid;
 
-    const int L = a.L;
+    // per-wave LDS: worklist, sorted new keys, output-slot bitmap, candidate
+    // ids and distances, visited table; sized for the widest phase of the launch
     unsigned char *mine = smem + (size_t)wid * a.lds_per_wave;
-    uint64_t *beam = reinterpret_cast<uint64_t *>(mine);
-    uint64_t *nkey = beam + L;                                   // 64
-    uint32_t *npos = reinterpret_cast<uint32_t *>(nkey + 64);    // 64
-    uint32_t *cid = npos + 64;                                   // 64
+    // (sizes keep every array 16-byte aligned: Lb and the bitmap word count are even)
+    const int Lb = (a.L_alloc + 1) & ~1;
+    const int pw = ((a.L_alloc >> 6) + 3) & ~1;
+    uint64_t *beam = reinterpret_cast<uint64_t *>(mine);         // Lb
+    uint64_t *nkey = beam + Lb;                                  // 64
+    uint64_t *posbm = nkey + 64;                                 // pw >= L/64 + 2
+    uint32_t *cid = reinterpret_cast<uint32_t *>(posbm + pw);   // 64
     float *cd = reinterpret_cast<float *>(cid + 64);             // 64
     uint32_t *htab = reinterpret_cast<uint32_t *>(cd + 64);      // H
 
     const IndexView ix = a.ix;
     const int R = ix.R, d = ix.d, m = ix.m;
 
-    uint32_t nA = bcast0(*a.n_active);
-    if (a.t_end < nA) nA = a.t_end;
-    if (*a.n_active <= a.tau_count) return;   // the loop of Alg. 1 has stopped
+    const uint32_t n_in = bcast0(*a.n_active);
+    if (n_in <= a.tau_count) return;   // the loop of Alg. 1 has stopped
+    const uint32_t nA = a.t_end < n_in ? a.t_end : n_in;
 
     Visited vs;
     vs.lds = htab;
     vs.lmask = (1u << a.h_log2) - 1u;
     vs.lshift = 32u - a.h_log2;
-    vs.gt = a.gtab + (size_t)slot * (1ull << a.g_log2);
-    vs.gmask = (1u << a.g_log2) - 1u;
-    vs.gshift = 32u - a.g_log2;
-    vs.epoch = bcast0(a.epochs[slot]);
-    if (vs.epoch == 0u || vs.epoch > 255u) vs.epoch = 1u;   // epoch 0 marks a zeroed table
+    vs.words32 = a.bits_words;
+    vs.bits = a.bits + (size_t)slot * a.bits_words;
     vs.status = a.status;
     const uint32_t spill_at = (1u << a.h_log2) >> 1;
 
     Scorer sc;
+#ifdef BOA_STAGE_PROFILE
+    uint64_t prof_acc[BOA_PROF_SLOTS] = {};
+#endif
     for (;;) {
         uint32_t t = 0;
         if (lane == 0) t = atomicAdd(a.queue, 1u);
@@ -351,36 +364,47 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             lo[j] = j < m ? a.ranges[((size_t)qi * m + j) * 2 + 0] : 0;
             hi[j] = j < m ? a.ranges[((size_t)qi * m + j) * 2 + 1] : 0;
         }
-        for (uint32_t i = lane; i < (1u << a.h_log2); i += 64) htab[i] = 0u;
+        // the phases of this launch: each restarts the search from the entry
+        // point at its own width (Alg. 1 calls Alg. 2 afresh)
+        for (int p = a.p_begin; p < a.p_end; ++p) {
+        const int L = a.sched[p];
+        {
+            uint4 z = make_uint4(0, 0, 0, 0);
+            uint4 *h4 = reinterpret_cast<uint4 *>(htab);
+            for (uint32_t i = lane; i < (vs.lmask + 1u) >> 2; i += 64) h4[i] = z;
+        }
         wave_sync();
 
-        bool spill = false, used_global = false;
+        bool spill = false;
         uint32_t lds_count = 0;
         uint32_t E = 0, S = 0;
-        uint32_t len = 0, scan_from = 0;
+        uint32_t len = 0;
         int expanded_j = -1;
+        // adjacency row already in flight for the node expected next
+        uint32_t pf_id = BOA_PAD;
+        uint64_t pf_key = KEY_NONE;
+        uint32_t pf_row = BOA_PAD;
 
         // the entry point is scored and entered before the first expansion
-        uint32_t c = 0;
-        {
-            uint32_t s = ix.entry;
-            if (lane == 0) {
-                visit_lds(vs, s);
-                cid[0] = s;
-            }
-            lds_count = 1;
-            c = 1;
+        uint32_t c = 1;
+        if (lane == 0) {
+            visit_lds(vs, ix.entry);
+            cid[0] = ix.entry;
         }
+        lds_count = 1;
 
         for (;;) {
+            uint32_t scan_from = (uint32_t)(expanded_j + 1);
             // ---- score the c new candidates listed in cid[0, c)
+            PROF_T(t_score0);
             if (c > 0) {
                 wave_sync();
                 S += c;
-                uint32_t phi = 0;
+                // attribute records first, then the vectors, so that both
+                // gathers are in flight together; phi is counted afterwards
+                int4 w0 = make_int4(0, 0, 0, 0), w1 = make_int4(0, 0, 0, 0);
                 if (lane < (int)c) {
                     const int32_t *ar = ix.attrs + (size_t)cid[lane] * ix.m_pad;
-                    int4 w0 = make_int4(0, 0, 0, 0), w1 = make_int4(0, 0, 0, 0);
                     if (ix.m_pad >= 4) {
                         w0 = reinterpret_cast<const int4 *>(ar)[0];
                         if (ix.m_pad == 8) w1 = reinterpret_cast<const int4 *>(ar)[1];
@@ -391,6 +415,10 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                     } else {
                         w0.x = ar[0];
                     }
+                }
+                sc.score(a.ix.vectors, d, cid, (int)c, cd, lane);
+                uint32_t phi = 0;
+                {
                     const int32_t av[BOA_MAX_M] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
 #pragma unroll
                     for (int j = 0; j < BOA_MAX_M; ++j) {
@@ -406,137 +434,187 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                         }
                     }
                 }
-                sc.score(a.ix.vectors, d, cid, (int)c, cd, lane);
                 wave_sync();
+                PROF_T(t_score1);
+                PROF_ADD(2, t_score1 - t_score0);
 
                 uint64_t key = KEY_NONE;
                 if (lane < (int)c) key = make_key(phi, cd[lane], cid[lane]);
-                if (len == (uint32_t)L) {
-                    uint64_t kth = beam[L - 1];
-                    if (key >= kth) key = KEY_NONE;   // cannot enter the worklist
-                }
-                uint64_t keep = __ballot(key != KEY_NONE);
-                uint32_t kept = __popcll(keep);
-                uint32_t next_scan = expanded_j + 1;
+                if (len == (uint32_t)L && key >= beam[L - 1]) key = KEY_NONE;  // cannot enter
+                const uint64_t keep = __ballot(key != KEY_NONE);
+                const uint32_t kept = __popcll(keep);
                 if (kept > 0) {
-                    key = wave_sort64(key, lane);
+                    // compact the survivors into lanes [0, kept) and sort them
+                    if (key != KEY_NONE) nkey[lanes_below(keep)] = key;
+                    wave_sync();
+                    key = lane < (int)kept ? nkey[lane] : KEY_NONE;
+                    uint32_t W = 1;
+                    while (W < kept) W <<= 1;
+                    key = wave_sort64(key, lane, W);
+                    if (lane < (int)kept) nkey[lane] = key;
+                    // the next node is the smaller of the best new key and the
+                    // entry predicted at selection: start its row load now
+                    {
+                        const uint64_t k0 = __shfl(key, 0);
+                        if (k0 < pf_key) {
+                            pf_key = k0;
+                            pf_id = key_id(k0);
+                            pf_row = lane < R ? ix.adj[(size_t)pf_id * R + lane] : BOA_PAD;
+                            PROF_ADD(9, 1);
+                        }
+                    }
+                    PROF_T(t_sort1);
+                    PROF_ADD(3, t_sort1 - t_score1);
+                    // rank of each new key in the worklist and its output slot
+                    uint32_t f = 0xFFFFFFFFu;
                     uint32_t pos = 0;
                     if (lane < (int)kept) {
                         pos = lower_bound64(beam, len, key);
-                        nkey[lane] = key;
-                        npos[lane] = pos;
+                        f = pos + lane;
                     }
+                    const uint32_t p0 = bcast0(pos);
+                    const uint32_t newlen = min((uint32_t)L, len + kept);
+                    const uint32_t w_lo = p0 >> 6, w_hi = (newlen - 1u) >> 6;
+                    for (uint32_t w = w_lo + lane; w <= w_hi; w += 64) posbm[w] = 0ull;
                     wave_sync();
-                    const uint32_t p0 = npos[0];
-                    // shift the suffix [p0, len) right; last chunk first
-                    if (len > p0) {
-                        int b = (int)(((len - 1) >> 6) << 6);
-                        int bmin = (int)((p0 >> 6) << 6);
-                        for (; b >= bmin; b -= 64) {
-                            uint32_t i = (uint32_t)b + lane;
-                            uint64_t val = 0;
-                            uint32_t dst = 0xFFFFFFFFu;
-                            if (i >= p0 && i < len) {
-                                val = beam[i];
-                                dst = i + upper_bound32(npos, kept, i);
-                            }
-                            wave_sync();
-                            if (dst < (uint32_t)L) beam[dst] = val;
-                            wave_sync();
+                    const bool placed = f < (uint32_t)L;
+                    if (placed) atomicOr(reinterpret_cast<unsigned long long *>(&posbm[f >> 6]),
+                                         1ull << (f & 63u));
+                    const uint32_t n_placed = __popcll(__ballot(placed));
+                    wave_sync();
+                    PROF_T(t_rank1);
+                    PROF_ADD(4, t_rank1 - t_sort1);
+                    PROF_ADD(7, w_hi - w_lo + 1);
+                    // rebuild [p0, newlen) from the last 64-slot chunk down
+                    uint64_t word = posbm[w_hi];
+                    uint32_t below = n_placed - (uint32_t)__popcll(word);   // new keys before chunk
+                    for (int w = (int)w_hi; w >= (int)w_lo; --w) {
+                        const uint32_t o = ((uint32_t)w << 6) + lane;
+                        const bool act = o >= p0 && o < newlen;
+                        const bool isnew = (word >> lane) & 1ull;
+                        const uint32_t cnt = below + (uint32_t)__popcll(word & ((1ull << lane) - 1ull));
+                        uint64_t val = 0;
+                        if (act) val = isnew ? nkey[cnt] : beam[o - cnt];
+                        wave_sync();
+                        if (act) beam[o] = val;
+                        if (w > (int)w_lo) {
+                            word = posbm[w - 1];
+                            below -= (uint32_t)__popcll(word);
                         }
+                        wave_sync();
                     }
-                    if (lane < (int)kept) {
-                        uint32_t dst = pos + lane;
-                        if (dst < (uint32_t)L) beam[dst] = key;
-                    }
-                    len = min((uint32_t)L, len + kept);
-                    if (p0 < next_scan) next_scan = p0;
-                    wave_sync();
+                    len = newlen;
+                    if (p0 < scan_from) scan_from = p0;
+                    PROF_T(t_merge1);
+                    PROF_ADD(5, t_merge1 - t_rank1);
                 }
-                scan_from = next_scan;
-            } else {
-                scan_from = expanded_j + 1;
             }
+            PROF_T(t_sel0);
 
-            // ---- select the nearest unexpanded entry
-            int j = -1;
-            for (uint32_t b = scan_from; b < len; b += 64) {
-                uint32_t i = b + lane;
+            // ---- select the nearest unexpanded entry (and predict the one after it)
+            int j = -1, j2 = -1;
+            for (uint32_t b0 = scan_from; b0 < len; b0 += 64) {
+                uint32_t i = b0 + lane;
                 bool un = (i < len) && !(beam[i] & 1ull);
                 uint64_t mk = __ballot(un);
                 if (mk) {
-                    j = (int)(b + __ffsll((unsigned long long)mk) - 1);
+                    j = (int)(b0 + __ffsll((unsigned long long)mk) - 1);
+                    uint64_t rest = mk & (mk - 1ull);
+                    if (rest) j2 = (int)(b0 + __ffsll((unsigned long long)rest) - 1);
                     break;
                 }
             }
             if (j < 0) break;   // converged: every entry expanded
+            PROF_T(t_sel1);
+            PROF_ADD(0, t_sel1 - t_sel0);
             expanded_j = j;
             const uint64_t ku = beam[j];
+            const uint64_t kn = j2 >= 0 ? beam[j2] : KEY_NONE;
             wave_sync();
             if (lane == 0) beam[j] = ku | 1ull;
             const uint32_t u = key_id(ku);
             E += 1;
 
-            // ---- gather the adjacency row and test-and-insert into the visited set
-            uint32_t v = lane < R ? ix.adj[(size_t)u * R + lane] : BOA_PAD;
+            // ---- adjacency row (prefetched if predicted), then the next prediction
+            uint32_t v;
+            if (u == pf_id) {
+                v = pf_row;
+                PROF_ADD(8, 1);
+            } else {
+                v = lane < R ? ix.adj[(size_t)u * R + lane] : BOA_PAD;
+            }
+            pf_key = kn;
+            pf_id = BOA_PAD;
+            if (j2 >= 0) {
+                pf_id = key_id(kn);
+                pf_row = lane < R ? ix.adj[(size_t)pf_id * R + lane] : BOA_PAD;
+            }
+            PROF_ADD(10, 1);
+
+            // ---- test-and-insert into the visited set
             if (!spill && lds_count + (uint32_t)R > spill_at) {
                 spill = true;
-                used_global = true;
+                clear_bits(vs, lane);
             }
             bool is_new = false;
             if (v != BOA_PAD) {
                 if (!spill) is_new = visit_lds(vs, v);
-                else is_new = !in_lds(vs, v) && visit_global(vs, v);
+                else is_new = !in_lds(vs, v) && visit_bits(vs, v);
             }
-            uint64_t nm = __ballot(is_new);
+            const uint64_t nm = __ballot(is_new);
             c = __popcll(nm);
             if (!spill) lds_count += c;
             if (is_new) cid[lanes_below(nm)] = v;
+            PROF_T(t_vis1);
+            PROF_ADD(1, t_vis1 - t_sel1);
+            PROF_ADD(6, spill ? 1 : 0);
         }
 
-        // ---- epilogue: result, phase width, confidence (Eq. 3)
+        // ---- epilogue: confidence (Eq. 3); the result is written by the
+        // last phase the query runs in this launch
         wave_sync();
         const uint32_t n_valid = lower_bound64(beam, len, KEY_PHI1);
         const int k = a.k;
-        for (int q = lane; q < k; q += 64) {
-            uint32_t id = BOA_PAD;
-            float dd = __int_as_float(0x7f800000);
-            if ((uint32_t)q < n_valid) {
-                uint64_t kk = beam[q];
-                id = key_id(kk);
-                dd = key_dist(kk);
-            }
-            a.ids[(size_t)qi * k + q] = id;
-            a.dists[(size_t)qi * k + q] = dd;
+        uint32_t conf = 0;
+        if (n_valid > (uint32_t)k) {
+            double dk = sqrt((double)key_dist(beam[k - 1]));
+            double dmax = sqrt((double)key_dist(beam[n_valid - 1]));
+            double gamma = dmax == 0.0 ? 0.0 : (dmax - dk) / dmax;
+            conf = gamma <= a.eps ? 1u : 0u;
         }
+        const bool last = conf != 0u || p + 1 == a.p_end;
         if (lane == 0) {
-            a.final_L[qi] = L;
-            uint32_t conf = 0;
-            if (n_valid > (uint32_t)k) {
-                double dk = sqrt((double)key_dist(beam[k - 1]));
-                double dmax = sqrt((double)key_dist(beam[n_valid - 1]));
-                double gamma = dmax == 0.0 ? 0.0 : (dmax - dk) / dmax;
-                conf = gamma <= a.eps ? 1u : 0u;
-            }
-            a.conf[t] = (uint8_t)conf;
-            a.qstat[qi] = (uint8_t)(1u + conf + (used_global ? 4u : 0u));
-            a.qE[qi] = E;
-            a.qS[qi] = S;
+            const size_t ps = (size_t)p * a.nq + qi;
+            a.qstat[ps] = (uint8_t)(1u + conf + (spill ? 4u : 0u));
+            a.qE[ps] = E;
+            a.qS[ps] = S;
             if (a.user_E) a.user_E[qi] += E;
             if (a.user_S) a.user_S[qi] += S;
+            if (a.p_end - a.p_begin == 1) a.conf[t] = (uint8_t)conf;
+            if (last) a.final_L[qi] = L;
         }
-        if (used_global) {
-            vs.epoch += 1u;
-            if (vs.epoch == 256u) {   // wrap: clear this wave's table
-                uint4 z = make_uint4(0, 0, 0, 0);
-                uint4 *g4 = reinterpret_cast<uint4 *>(vs.gt);
-                for (uint32_t i = lane; i < ((vs.gmask + 1u) >> 2); i += 64) g4[i] = z;
-                vs.epoch = 1u;
+        if (last) {
+            for (int q = lane; q < k; q += 64) {
+                uint32_t id = BOA_PAD;
+                float dd = __int_as_float(0x7f800000);
+                if ((uint32_t)q < n_valid) {
+                    uint64_t kk = beam[q];
+                    id = key_id(kk);
+                    dd = key_dist(kk);
+                }
+                a.ids[(size_t)qi * k + q] = id;
+                a.dists[(size_t)qi * k + q] = dd;
             }
         }
         wave_sync();
+        if (last) break;
+        }   // phases
+    }       // queries
+#ifdef BOA_STAGE_PROFILE
+    if (lane == 0 && a.prof) {
+        for (int i = 0; i < BOA_PROF_SLOTS; ++i) a.prof[(size_t)slot * BOA_PROF_SLOTS + i] += prof_acc[i];
     }
-    if (lane == 0) a.epochs[slot] = vs.epoch;
+#endif
 }
 
 // Stable compaction of the active list (Alg. 1: survivors escalate). One

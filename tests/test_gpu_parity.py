@@ -58,12 +58,13 @@ def tiny():
                 gpu=boa.Index(data.vectors, data.attrs, types, adj, entry))
 
 
-def test_tiny_adaptive(tiny):
+@pytest.mark.parametrize("fused", [False, True])
+def test_tiny_adaptive(tiny, fused):
     wl, d = tiny["wl"], tiny["data"]
     sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
     ref = oracle.boa(tiny["orc"], d.queries, d.ranges, wl.k, sched)
-    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax)
-    assert_parity(got, ref, "tiny adaptive")
+    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax, fused=fused)
+    assert_parity(got, ref, f"tiny adaptive fused={fused}")
     st = tiny["gpu"].stats()
     assert [p["L"] for p in st["phases"]] == sched
     for p, rp in zip(st["phases"], ref.phases):
@@ -79,28 +80,34 @@ def test_tiny_fixed_width(tiny, L):
     assert_parity(got, ref, f"tiny fixed L={L}")
 
 
-@pytest.mark.parametrize("slots", [64, 256])
-def test_forced_spill_changes_nothing(tiny, slots):
-    """A tiny LDS visited table sends almost every insert to the HBM table."""
+@pytest.mark.parametrize("slots,fused", [(64, False), (256, False), (64, True)])
+def test_forced_spill_changes_nothing(tiny, slots, fused):
+    """A tiny LDS visited table sends almost every insert to the HBM bitmap."""
     wl, d = tiny["wl"], tiny["data"]
     sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
     ref = oracle.boa(tiny["orc"], d.queries, d.ranges, wl.k, sched)
     got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax,
-                     lds_hash_slots=slots)
+                     lds_hash_slots=slots, fused=fused)
     assert_parity(got, ref, f"spill slots={slots}")
     assert tiny["gpu"].stats()["spilled_queries"] > 0
-    # and twice in a row: the wave-slot epochs must isolate the searches
+    # and twice in a row: a wave slot's bitmap is reset by the next query that spills
     got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax,
-                     lds_hash_slots=slots)
+                     lds_hash_slots=slots, fused=fused)
     assert_parity(got, ref, f"spill slots={slots}, repeated")
 
 
-def test_paper_schedule(tiny):
+@pytest.mark.parametrize("fused", [False, True])
+def test_paper_schedule(tiny, fused):
     """The paper's experiments use widths 10, 100, 200 (Sec. IV)."""
     wl, d = tiny["wl"], tiny["data"]
     ref = oracle.boa(tiny["orc"], d.queries, d.ranges, 10, [10, 100, 200], eps=0.02)
-    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=10, schedule=[10, 100, 200], eps=0.02)
+    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=10, schedule=[10, 100, 200], eps=0.02,
+                     fused=fused)
     assert_parity(got, ref, "schedule 10/100/200")
+    st = tiny["gpu"].stats()
+    for p, rp in zip(st["phases"], ref.phases):
+        assert (p["active"], p["confident"], p["expansions"], p["scored"]) == \
+            (rp["active"], rp["confident"], rp["expansions"], rp["scored"])
 
 
 def test_single_query_equals_batch(tiny):
@@ -156,6 +163,8 @@ def test_no_queries(tiny):
         tiny["gpu"].search(q, r, k=10, tau=1.0)
     with pytest.raises(boa.BoaError):
         tiny["gpu"].search(q, r, k=10, lds_hash_slots=100)
+    with pytest.raises(boa.BoaError):
+        tiny["gpu"].search(q, r, k=10, tau=0.1, fused=True)
 
 
 # ---------------------------------------------------------------------------
@@ -190,6 +199,8 @@ def test_shapes(shape):
     ref = oracle.boa(orc, q, r, 10, sched, eps=0.1)
     got = gpu_search(gpu, q, r, k=10, L0=16, Lmax=256, eps=0.1)
     assert_parity(got, ref, f"shape {shape}")
+    got = gpu_search(gpu, q, r, k=10, L0=16, Lmax=256, eps=0.1, fused=True)
+    assert_parity(got, ref, f"shape {shape} fused")
     ref = oracle.boa(orc, q, r, 10, [300])
     got = gpu_search(gpu, q, r, k=10, fixed_L=300, lds_hash_slots=2 * 64 if R < 64 else 256)
     assert_parity(got, ref, f"shape {shape} fixed 300 with spill")
