@@ -74,7 +74,8 @@ enum { BOA_ATTR_I32 = 0, BOA_ATTR_F32 = 1 };
  *   attr_dtypes host, m entries of BOA_ATTR_I32 / BOA_ATTR_F32.
  *   adjacency   host, row-major n x R uint32 neighbour ids, padded with
  *               0xFFFFFFFF; 1 <= R <= BOA_MAX_R. A row may not hold its own
- *               id. (Graph construction is an offline step: Sec. II.)
+ *               id, nor any id twice. (Graph construction is an offline step:
+ *               Sec. II.)
  *   entry       the entry point s of every search (Alg. 2), 0 <= entry < n.
  *   n           1 <= n < BOA_MAX_N.
  *   out         receives the index; free it with boa_free_index.
@@ -99,8 +100,10 @@ typedef struct {
                                fixed-beamwidth baseline); overrides L0/Lmax/schedule */
     int32_t boa_plus;       /* 1: BOA+ sub-batched first phase overlapped with escalation */
     int32_t sub_batches;    /* BOA+ first-phase sub-batches; default 10 */
-    int32_t lds_hash_slots; /* 0: automatic; else a power of two >= 64 that forces the
-                               per-wave LDS visited-table size (tests force spills) */
+    int32_t lds_hash_slots; /* 0: automatic; else a power of two in [64, 16384] that forces
+                               the 16-bit slots of the per-wave LDS visited table (tests
+                               force spills to the HBM bitmap); at least 8 * 2^(B-14)
+                               for ids of B bits */
     const int32_t *schedule; /* optional host array of explicit phase widths
                                 (strictly increasing); overrides L0/Lmax/alpha */
     int32_t n_schedule;

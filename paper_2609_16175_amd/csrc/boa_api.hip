@@ -188,10 +188,21 @@ int boa_build_index_from_arrays(const void *vectors, int64_t n, int32_t d, int32
         if (attr_dtypes[j] == BOA_ATTR_F32) f32_mask |= 1u << j;
         else if (attr_dtypes[j] != BOA_ATTR_I32) return fail(BOA_EINVAL, "bad attribute dtype");
     }
-    for (int64_t i = 0; i < n * (int64_t)R; ++i) {
-        uint32_t v = adjacency[i];
-        if (v != BOA_PAD && (int64_t)v >= n) return fail(BOA_EINVAL, "adjacency id out of range");
-        if (v != BOA_PAD && (int64_t)v == i / R) return fail(BOA_EINVAL, "adjacency row holds its own id");
+    {
+        std::vector<uint32_t> row((size_t)R);
+        for (int64_t u = 0; u < n; ++u) {
+            int cnt = 0;
+            for (int r = 0; r < R; ++r) {
+                uint32_t v = adjacency[u * R + r];
+                if (v == BOA_PAD) continue;
+                if ((int64_t)v >= n) return fail(BOA_EINVAL, "adjacency id out of range");
+                if ((int64_t)v == u) return fail(BOA_EINVAL, "adjacency row holds its own id");
+                row[cnt++] = v;
+            }
+            std::sort(row.begin(), row.begin() + cnt);
+            if (std::adjacent_find(row.begin(), row.begin() + cnt) != row.begin() + cnt)
+                return fail(BOA_EINVAL, "adjacency row holds an id twice");
+        }
     }
 
     boa_index *ix = new (std::nothrow) boa_index();
@@ -351,17 +362,34 @@ int make_schedule(const boa_params *p, std::vector<int32_t> &s)
     return BOA_OK;
 }
 
+uint32_t id_bits(const boa_index *ix)
+{
+    uint32_t b = 1;
+    while (b < 32 && ((int64_t)1 << b) < ix->view.n) ++b;
+    return b;
+}
+
+// 8 slots per bucket, at most 14 stored bits per id
+uint32_t min_table_slots(const boa_index *ix)
+{
+    const uint32_t B = id_bits(ix);
+    return std::max<uint32_t>(64u, B > 14 ? (8u << (B - 14)) : 64u);
+}
+
 PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t max_active)
 {
     PhasePlan pl{};
     pl.L = L;
-    // visited table: 2048 slots (8 KB) at every width. The wide phases hold
-    // few queries, so a small table keeps them all resident at once; what
-    // does not fit spills to the HBM bitmap.
-    uint32_t h = forced_h > 0 ? (uint32_t)forced_h : 2048u;
+    // visited table: 16-bit slots, 16 per expected scored node of a width-L
+    // search, between 1024 and 4096 (2-8 KB); ids that find both of their
+    // buckets full go to the HBM bitmap. The table must leave at most 14
+    // stored bits per id.
+    uint32_t h = forced_h > 0 ? (uint32_t)forced_h
+                              : std::min<uint32_t>(4096u, std::max<uint32_t>(1024u, next_pow2(16ull * L)));
+    h = std::max<uint32_t>(h, min_table_slots(ix));
     pl.h_slots = (int32_t)h;
     const int32_t Lb = (L + 1) & ~1, pw = ((L >> 6) + 3) & ~1;
-    pl.lds_per_wave = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + 4 * (int32_t)h;
+    pl.lds_per_wave = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + 2 * (int32_t)h;
     pl.lds_per_wave = (pl.lds_per_wave + 15) & ~15;
     // waves per block: the choice with the most resident waves per CU
     int best_w = 0, best_wpb = 1, best_occ = 1;
@@ -404,8 +432,8 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     if (p->lds_hash_slots && (p->lds_hash_slots < 64 || (p->lds_hash_slots & (p->lds_hash_slots - 1)) ||
                               p->lds_hash_slots > 16384))
         return fail(BOA_EINVAL, "lds_hash_slots must be 0 or a power of two in [64, 16384]");
-    if (p->lds_hash_slots && (uint32_t)p->lds_hash_slots / 2 < (uint32_t)ix->view.R + 1)
-        return fail(BOA_EINVAL, "lds_hash_slots too small for the graph degree");
+    if (p->lds_hash_slots && (uint32_t)p->lds_hash_slots < min_table_slots(ix))
+        return fail(BOA_EINVAL, "lds_hash_slots too small for this index's id width");
     const bool plus = p->boa_plus != 0 && p->fixed_L <= 0;
     const bool fused = p->fused != 0;
     if (fused && p->tau != 0.0)
@@ -465,6 +493,7 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     base.user_S = scored;
     base.bits = ix->bits;
     base.bits_words = ix->bits_words;
+    base.id_bits = id_bits(ix);
     base.status = ix->status;
     base.eps = p->eps;
     base.tau_count = tau_count;

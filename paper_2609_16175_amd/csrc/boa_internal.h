@@ -49,7 +49,8 @@ struct PhaseArgs {
     int32_t sched[BOA_MAX_PHASES]; // phase widths
     int32_t p_begin, p_end;   // phases run by this launch (one, or all when fused)
     int32_t L_alloc;          // widest of them: sizes the per-wave LDS
-    int32_t h_log2;
+    int32_t h_log2;           // log2 of the LDS visited-table slots (16-bit entries)
+    uint32_t id_bits;         // bits of the largest id (ceil(log2 n))
     int32_t lds_per_wave, waves_per_block;
     uint32_t slot_base;
     unsigned long long *prof; // per wave slot: BOA_PROF_SLOTS stage counters (profiling builds)

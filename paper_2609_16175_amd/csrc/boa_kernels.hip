@@ -246,49 +246,80 @@ struct U8Scorer {
 };
 
 // ---------------------------------------------------------------------------
-// Visited set. LDS table: open addressing with linear probing, 0 = empty,
-// else id + 1. Once half full, new ids go to the wave slot's bitmap over
-// all points in HBM (one bit per point), zeroed when a query first spills;
-// every probe then checks the LDS table first and the bitmap second.
+// Visited set (exact). LDS part: a two-choice bucketed table of 16-bit
+// entries. A bijective mix of the id's B bits gives h; its top bits select
+// the home bucket b1, the low r = B - log2(buckets) <= 14 bits are stored.
+// The alternate bucket is b2 = b1 ^ alt(r) (alt odd, so b2 != b1). An entry
+// is 0x8000 | r in b1 or 0xC000 | r in b2, so (bucket, entry) identifies the
+// id uniquely. A bucket holds 8 entries (16 bytes, one LDS read).
+// Insert goes to the emptier bucket through a 32-bit CAS on the word that
+// holds the slot. When both buckets are full the id goes to the wave slot's
+// bitmap over all points in HBM (zeroed when a query first overflows).
+// Buckets only fill up, so an id absent from a bucket pair that still has
+// room has never been inserted anywhere: the bitmap is consulted only when
+// both buckets are full.
 
 struct Visited {
-    uint32_t *lds;
-    uint32_t lmask, lshift;
-    uint32_t *bits;      // this wave slot's bitmap, words32 words
+    uint32_t *words;     // LDS table, 2 entries per word, 4 words per bucket
+    uint32_t bmask;      // buckets - 1
+    uint32_t rbits;      // stored bits per id
+    uint32_t idbits;     // B
+    uint32_t *bits;      // this wave slot's HBM bitmap, words32 words
     uint32_t words32;
     uint32_t *status;
 };
 
-// true if v was not in the set (and is now)
-__device__ __forceinline__ bool visit_lds(const Visited &s, uint32_t v)
+__device__ __forceinline__ uint32_t mix_id(uint32_t v, uint32_t B)
 {
-    uint32_t key = v + 1u;
-    uint32_t h = hash32(v) >> s.lshift;
-    for (uint32_t probe = 0; probe <= s.lmask; ++probe) {
-        uint32_t cur = s.lds[h];
-        if (cur == key) return false;
-        if (cur == 0u) {
-            uint32_t old = atomicCAS(&s.lds[h], 0u, key);
-            if (old == 0u) return true;
-            if (old == key) return false;
-        }
-        h = (h + 1u) & s.lmask;
-    }
-    atomicOr(s.status, BOA_STATUS_OVERFLOW);
-    return false;
+    const uint32_t mask = B >= 32 ? 0xFFFFFFFFu : ((1u << B) - 1u);
+    uint32_t h = (v * 0x9E3779B1u) & mask;
+    h ^= h >> ((B + 1u) >> 1);
+    return (h * 0x85EBCA6Bu) & mask;
 }
 
-__device__ __forceinline__ bool in_lds(const Visited &s, uint32_t v)
+__device__ __forceinline__ bool has16(const uint4 &b, uint32_t e)
 {
-    uint32_t key = v + 1u;
-    uint32_t h = hash32(v) >> s.lshift;
-    for (uint32_t probe = 0; probe <= s.lmask; ++probe) {
-        uint32_t cur = s.lds[h];
-        if (cur == key) return true;
-        if (cur == 0u) return false;
-        h = (h + 1u) & s.lmask;
+    return ((b.x & 0xFFFFu) == e) | ((b.x >> 16) == e) | ((b.y & 0xFFFFu) == e) | ((b.y >> 16) == e) |
+           ((b.z & 0xFFFFu) == e) | ((b.z >> 16) == e) | ((b.w & 0xFFFFu) == e) | ((b.w >> 16) == e);
+}
+
+__device__ __forceinline__ uint32_t empties16(const uint4 &b)
+{
+    return ((b.x & 0xFFFFu) == 0u) + ((b.x >> 16) == 0u) + ((b.y & 0xFFFFu) == 0u) + ((b.y >> 16) == 0u) +
+           ((b.z & 0xFFFFu) == 0u) + ((b.z >> 16) == 0u) + ((b.w & 0xFFFFu) == 0u) + ((b.w >> 16) == 0u);
+}
+
+// 1: v was not in the set and now is (in LDS); 0: v was already there;
+// -1: both buckets full and v not in them (the caller consults the bitmap).
+__device__ __forceinline__ int visit_lds(const Visited &s, uint32_t v)
+{
+    const uint32_t h = mix_id(v, s.idbits);
+    const uint32_t r = h & ((1u << s.rbits) - 1u);
+    const uint32_t b1 = h >> s.rbits;
+    const uint32_t b2 = (b1 ^ (((r * 0x5BD1E995u + 0x7F4A7C15u) >> 7) | 1u)) & s.bmask;
+    const uint32_t e1 = 0x8000u | r, e2 = 0xC000u | r;
+    const uint4 *bk = reinterpret_cast<const uint4 *>(s.words);
+    for (int attempt = 0; attempt < 256; ++attempt) {
+        const uint4 B1 = bk[b1], B2 = bk[b2];
+        if (has16(B1, e1) || has16(B2, e2)) return 0;
+        const uint32_t n1 = empties16(B1), n2 = empties16(B2);
+        if (n1 == 0u && n2 == 0u) return -1;
+        const bool use1 = n1 >= n2;
+        const uint4 Bc = use1 ? B1 : B2;
+        const uint32_t e = use1 ? e1 : e2;
+        const uint32_t bi = use1 ? b1 : b2;
+        const uint32_t w[4] = {Bc.x, Bc.y, Bc.z, Bc.w};
+        uint32_t wi = 0, old = 0, neu = 0;
+#pragma unroll
+        for (int q = 3; q >= 0; --q) {   // first (lowest) free half-word
+            if ((w[q] >> 16) == 0u) { wi = q; old = w[q]; neu = w[q] | (e << 16); }
+            if ((w[q] & 0xFFFFu) == 0u) { wi = q; old = w[q]; neu = w[q] | e; }
+        }
+        if (atomicCAS(&s.words[bi * 4u + wi], old, neu) == old) return 1;
+        // another lane changed that word: look again
     }
-    return false;
+    atomicOr(s.status, BOA_STATUS_OVERFLOW);
+    return 0;
 }
 
 __device__ __forceinline__ bool visit_bits(const Visited &s, uint32_t v)
@@ -328,7 +359,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     uint64_t *posbm = nkey + 64;                                 // pw >= L/64 + 2
     uint32_t *cid = reinterpret_cast<uint32_t *>(posbm + pw);   // 64
     float *cd = reinterpret_cast<float *>(cid + 64);             // 64
-    uint32_t *htab = reinterpret_cast<uint32_t *>(cd + 64);      // H
+    uint32_t *htab = reinterpret_cast<uint32_t *>(cd + 64);      // H/2 words (H 16-bit slots)
 
     const IndexView ix = a.ix;
     const int R = ix.R, d = ix.d, m = ix.m;
@@ -338,13 +369,14 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     const uint32_t nA = a.t_end < n_in ? a.t_end : n_in;
 
     Visited vs;
-    vs.lds = htab;
-    vs.lmask = (1u << a.h_log2) - 1u;
-    vs.lshift = 32u - a.h_log2;
+    vs.words = htab;
+    vs.bmask = (1u << (a.h_log2 - 3)) - 1u;       // 8 slots per bucket
+    vs.idbits = a.id_bits;
+    vs.rbits = a.id_bits > (uint32_t)(a.h_log2 - 3) ? a.id_bits - (uint32_t)(a.h_log2 - 3) : 0u;
     vs.words32 = a.bits_words;
     vs.bits = a.bits + (size_t)slot * a.bits_words;
     vs.status = a.status;
-    const uint32_t spill_at = (1u << a.h_log2) >> 1;
+    const uint32_t table_words = (1u << a.h_log2) >> 1;
 
     Scorer sc;
 #ifdef BOA_STAGE_PROFILE
@@ -371,12 +403,11 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         {
             uint4 z = make_uint4(0, 0, 0, 0);
             uint4 *h4 = reinterpret_cast<uint4 *>(htab);
-            for (uint32_t i = lane; i < (vs.lmask + 1u) >> 2; i += 64) h4[i] = z;
+            for (uint32_t i = lane; i < table_words >> 2; i += 64) h4[i] = z;
         }
         wave_sync();
 
         bool spill = false;
-        uint32_t lds_count = 0;
         uint32_t E = 0, S = 0;
         uint32_t len = 0;
         int expanded_j = -1;
@@ -391,7 +422,6 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             visit_lds(vs, ix.entry);
             cid[0] = ix.entry;
         }
-        lds_count = 1;
 
         for (;;) {
             uint32_t scan_from = (uint32_t)(expanded_j + 1);
@@ -552,18 +582,18 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             PROF_ADD(10, 1);
 
             // ---- test-and-insert into the visited set
-            if (!spill && lds_count + (uint32_t)R > spill_at) {
-                spill = true;
-                clear_bits(vs, lane);
+            int vst = 0;
+            if (v != BOA_PAD) vst = visit_lds(vs, v);
+            if (__ballot(vst < 0) != 0ull) {
+                if (!spill) {          // first overflow of this query: reset the bitmap
+                    spill = true;
+                    clear_bits(vs, lane);
+                }
+                if (vst < 0) vst = visit_bits(vs, v) ? 1 : 0;
             }
-            bool is_new = false;
-            if (v != BOA_PAD) {
-                if (!spill) is_new = visit_lds(vs, v);
-                else is_new = !in_lds(vs, v) && visit_bits(vs, v);
-            }
+            const bool is_new = vst > 0;
             const uint64_t nm = __ballot(is_new);
             c = __popcll(nm);
-            if (!spill) lds_count += c;
             if (is_new) cid[lanes_below(nm)] = v;
             PROF_T(t_vis1);
             PROF_ADD(1, t_vis1 - t_sel1);

@@ -70,6 +70,7 @@ def _build(**over):
     (dict(types=np.array([0, 5], np.int32)), "dtype"),
     (dict(adj=np.full((50, 4), 50, np.uint32)), "adjacency id out of range"),
     (dict(adj=np.tile(np.arange(50, dtype=np.uint32)[:, None], (1, 4))), "its own id"),
+    (dict(adj=np.tile(np.array([[30, 9, 30, 0xFFFFFFFF]], dtype=np.uint32), (50, 1))), "twice"),
 ])
 def test_build_validation(over, needle):
     rc, msg = _build(**over)
