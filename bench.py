@@ -215,8 +215,10 @@ def main():
         return (t1 - t0) * 1e3 / steps, index.stats(), o
 
     modes = {}
-    for mode in ("phased", "fused"):
-        ms_m, st_m, out_m = timed(dict(kw, fused=(mode == "fused")), args.steps, args.warmup)
+    mode_kw = {"phased": {}, "fused": {"fused": True},
+               "boa_plus": {"boa_plus": True, "sub_batches": wl.sub_batches}}
+    for mode in ("phased", "fused", "boa_plus"):
+        ms_m, st_m, out_m = timed(dict(kw, **mode_kw[mode]), args.steps, args.warmup)
         modes[mode] = (ms_m, st_m, out_m)
         log(f"adaptive ({mode}): {ms_m:.3f} ms/step, {wl.nq / (ms_m / 1e3):,.0f} QPS")
     mode = min(modes, key=lambda k2: modes[k2][0])

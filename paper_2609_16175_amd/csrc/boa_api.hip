@@ -109,6 +109,7 @@ struct boa_index {
     std::vector<PhasePlan> plans;
     std::vector<std::pair<int, int>> launch_phase;  // (phase, event index)
     hipEvent_t ev_all0 = nullptr, ev_all1 = nullptr;
+    hipEvent_t ev_pool = nullptr, ev_join = nullptr;   // BOA+ cross-stream ordering
     bool have_stats = false;
     int64_t cum_searches = 0, cum_launches = 0;
     double cum_kernel_ms = 0.0;
@@ -161,6 +162,8 @@ void boa_free_index(boa_index *ix)
     for (auto e : ix->ev_end) (void)hipEventDestroy(e);
     if (ix->ev_all0) (void)hipEventDestroy(ix->ev_all0);
     if (ix->ev_all1) (void)hipEventDestroy(ix->ev_all1);
+    if (ix->ev_pool) (void)hipEventDestroy(ix->ev_pool);
+    if (ix->ev_join) (void)hipEventDestroy(ix->ev_join);
     if (ix->aux) (void)hipStreamDestroy(ix->aux);
     (void)hipSetDevice(cur);
     delete ix;
@@ -297,7 +300,7 @@ int ensure_workspace(boa_index *ix, int64_t nq, int32_t n_phases, uint64_t slots
         if ((rc = dalloc(&ix->active[0], cap)) || (rc = dalloc(&ix->active[1], cap)) ||
             (rc = dalloc(&ix->conf, cap)) || (rc = dalloc(&ix->qstat, (size_t)cap * pc)) ||
             (rc = dalloc(&ix->qE, (size_t)cap * pc)) || (rc = dalloc(&ix->qS, (size_t)cap * pc)) ||
-            (rc = dalloc(&ix->pool, (size_t)cap * pc))) {
+            (rc = dalloc(&ix->pool, (size_t)cap * 2))) {
             ix->nq_cap = 0;
             ix->ph_cap = 0;
             return rc;
@@ -327,7 +330,11 @@ int ensure_workspace(boa_index *ix, int64_t nq, int32_t n_phases, uint64_t slots
         ix->slots_cap = sc;
         ix->bits_words = words;
     }
-    if (plus && !ix->aux) HIP_TRY(hipStreamCreateWithFlags(&ix->aux, hipStreamNonBlocking));
+    if (plus && !ix->aux) {
+        HIP_TRY(hipStreamCreateWithFlags(&ix->aux, hipStreamNonBlocking));
+        HIP_TRY(hipEventCreateWithFlags(&ix->ev_pool, hipEventDisableTiming));
+        HIP_TRY(hipEventCreateWithFlags(&ix->ev_join, hipEventDisableTiming));
+    }
     return BOA_OK;
 }
 
@@ -439,6 +446,8 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     if (fused && p->tau != 0.0)
         return fail(BOA_EINVAL, "fused phases need tau == 0 (the residual test counts all queries of a phase)");
     if (fused && plus) return fail(BOA_EINVAL, "fused and boa_plus are exclusive");
+    if (plus && p->tau != 0.0)
+        return fail(BOA_EINVAL, "BOA+ needs tau == 0 (the residual test counts all queries of a phase)");
     if (plus && (p->sub_batches < 1 || p->sub_batches > 1024)) return fail(BOA_EINVAL, "sub_batches out of range");
     if (nq == 0) return BOA_OK;
 
@@ -451,8 +460,9 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     std::vector<PhasePlan> plans;
     uint64_t slots = 0;
     for (int32_t ph = 0; ph < n_phases; ++ph) {
-        // a fused launch sizes its LDS for the widest phase
-        PhasePlan pl = plan_phase(ix, fused ? sched.back() : sched[ph], p->lds_hash_slots, nq);
+        // a fused launch, and a BOA+ escalation launch, size LDS for the widest phase
+        const bool wide = fused || (plus && ph > 0);
+        PhasePlan pl = plan_phase(ix, wide ? sched.back() : sched[ph], p->lds_hash_slots, nq);
         pl.L = sched[ph];
         if ((size_t)pl.lds_per_wave > ix->lds_per_block_max)
             return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
@@ -538,6 +548,7 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
             a.queue = ix->counters + ph;
             a.p_begin = ph;
             a.p_end = ph + 1;
+            a.write_conf = 1;
             a.L_alloc = pl.L;
             a.h_log2 = ilog2((uint32_t)pl.h_slots);
             a.lds_per_wave = pl.lds_per_wave;
@@ -585,7 +596,102 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
             }
         }
     } else {
-        return fail(BOA_EUNSUPPORTED, "BOA+ is not available in this build yet");
+        // BOA+ (Sec. III-A, "Pipelining Multiple Batches"): phase 0 runs as
+        // `sub` sub-batches on the caller's stream; the survivors of the
+        // first half are pooled and escalated through the remaining widths
+        // in one launch on a second stream while the second half of phase 0
+        // runs; the second half's pooled survivors follow on the caller's
+        // stream. Each escalation launch carries its queries through all
+        // remaining widths (results are those of BOA).
+        const int64_t B = (nq + sub - 1) / sub;
+        const int32_t nsub = (int32_t)((nq + B - 1) / B);
+        const int32_t half = (nsub + 1) / 2;
+        uint32_t *pool[2] = {ix->pool, ix->pool + nq};
+        uint32_t *pool_n[2] = {ix->n_active + BOA_MAX_PHASES + 1, ix->n_active + BOA_MAX_PHASES + 2};
+        PhasePlan &p0 = plans[0];
+        for (int32_t b = 0; b < nsub; ++b) {
+            PhaseArgs a = base;
+            a.active = ix->active[0];
+            a.n_active = ix->n_active;
+            a.t_begin = (uint32_t)(b * B);
+            a.t_end = (uint32_t)std::min<int64_t>(nq, (b + 1) * B);
+            a.queue = ix->counters + b;
+            a.p_begin = 0;
+            a.p_end = 1;
+            a.write_conf = 1;
+            a.L_alloc = sched[0];
+            a.h_log2 = ilog2((uint32_t)p0.h_slots);
+            a.lds_per_wave = p0.lds_per_wave;
+            a.waves_per_block = p0.wpb;
+            a.slot_base = 0;
+            const int64_t span = a.t_end - a.t_begin;
+            const int blocks = (int)std::min<int64_t>(p0.blocks, (span + p0.wpb - 1) / p0.wpb);
+            HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
+            HIP_TRY(launch_phase(a, ix->vec_dtype, blocks, st));
+            HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
+            ix->launch_phase.push_back({0, ev});
+            ++ev;
+            p0.launches += 1;
+            AppendArgs ap{};
+            ap.in = ix->active[0] + a.t_begin;
+            ap.conf = ix->conf + a.t_begin;
+            ap.n = (uint32_t)span;
+            const int g = b < half ? 0 : 1;
+            ap.pool = pool[g];
+            ap.pool_count = pool_n[g];
+            HIP_TRY(launch_append(ap, st));
+            if (b == half - 1 && n_phases > 1) {
+                // first pool complete: escalate it on the second stream
+                HIP_TRY(hipEventRecord(ix->ev_pool, st));
+                HIP_TRY(hipStreamWaitEvent(ix->aux, ix->ev_pool, 0));
+                PhasePlan &pe = plans[1];
+                PhaseArgs e = base;
+                e.active = pool[0];
+                e.n_active = pool_n[0];
+                e.t_begin = 0;
+                e.t_end = 0xFFFFFFFFu;
+                e.queue = ix->counters + nsub;
+                e.p_begin = 1;
+                e.p_end = n_phases;
+                e.L_alloc = sched.back();
+                e.h_log2 = ilog2((uint32_t)pe.h_slots);
+                e.lds_per_wave = pe.lds_per_wave;
+                e.waves_per_block = pe.wpb;
+                e.slot_base = (uint32_t)slots;   // disjoint spill bitmaps from stream 0
+                HIP_TRY(hipEventRecord(ix->ev_start[ev], ix->aux));
+                HIP_TRY(launch_phase(e, ix->vec_dtype, pe.blocks, ix->aux));
+                HIP_TRY(hipEventRecord(ix->ev_end[ev], ix->aux));
+                ix->launch_phase.push_back({1, ev});
+                ++ev;
+                pe.launches += 1;
+            }
+        }
+        if (n_phases > 1 && nsub > half) {
+            PhasePlan &pe = plans[1];
+            PhaseArgs e = base;
+            e.active = pool[1];
+            e.n_active = pool_n[1];
+            e.t_begin = 0;
+            e.t_end = 0xFFFFFFFFu;
+            e.queue = ix->counters + nsub + 1;
+            e.p_begin = 1;
+            e.p_end = n_phases;
+            e.L_alloc = sched.back();
+            e.h_log2 = ilog2((uint32_t)pe.h_slots);
+            e.lds_per_wave = pe.lds_per_wave;
+            e.waves_per_block = pe.wpb;
+            e.slot_base = 0;
+            HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
+            HIP_TRY(launch_phase(e, ix->vec_dtype, pe.blocks, st));
+            HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
+            ix->launch_phase.push_back({1, ev});
+            ++ev;
+            pe.launches += 1;
+        }
+        if (n_phases > 1) {
+            HIP_TRY(hipEventRecord(ix->ev_join, ix->aux));
+            HIP_TRY(hipStreamWaitEvent(st, ix->ev_join, 0));
+        }
     }
 
     HIP_TRY(hipEventRecord(ix->ev_all1, st));

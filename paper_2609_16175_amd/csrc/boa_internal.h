@@ -48,6 +48,7 @@ struct PhaseArgs {
     int32_t k;
     int32_t sched[BOA_MAX_PHASES]; // phase widths
     int32_t p_begin, p_end;   // phases run by this launch (one, or all when fused)
+    int32_t write_conf;       // record each query's confidence for a compaction/append
     int32_t L_alloc;          // widest of them: sizes the per-wave LDS
     int32_t h_log2;           // log2 of the LDS visited-table slots (16-bit entries)
     uint32_t id_bits;         // bits of the largest id (ceil(log2 n))
@@ -65,6 +66,14 @@ struct CompactArgs {
     uint32_t tau_count;
 };
 
+struct AppendArgs {
+    const uint32_t *in;       // slice of the active list
+    const uint8_t *conf;      // its confidence flags
+    uint32_t n;               // slice length
+    uint32_t *pool;           // destination pool
+    uint32_t *pool_count;     // its length (device; read, then advanced)
+};
+
 struct InitArgs {
     uint32_t *active0;
     uint32_t *n_active;
@@ -80,6 +89,7 @@ struct InitArgs {
 hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st);
 int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds);
 hipError_t launch_compact(const CompactArgs &a, hipStream_t st);
+hipError_t launch_append(const AppendArgs &a, hipStream_t st);
 hipError_t launch_init(const InitArgs &a, hipStream_t st);
 
 }  // namespace boa

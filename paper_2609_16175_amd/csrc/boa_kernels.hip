@@ -620,7 +620,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             a.qS[ps] = S;
             if (a.user_E) a.user_E[qi] += E;
             if (a.user_S) a.user_S[qi] += S;
-            if (a.p_end - a.p_begin == 1) a.conf[t] = (uint8_t)conf;
+            if (a.write_conf) a.conf[t] = (uint8_t)conf;
             if (last) a.final_L[qi] = L;
         }
         if (last) {
@@ -678,6 +678,36 @@ __global__ void __launch_bounds__(1024) compact_kernel(CompactArgs a)
     if (threadIdx.x == 0) *a.n_out = stopped ? 0u : base_s;
 }
 
+// BOA+ survivor pooling: append the non-confident entries of one phase-0
+// sub-batch (a slice of the active list) to a pool, stably, after the
+// pool's current entries; then publish the new count. One block.
+__global__ void __launch_bounds__(1024) append_kernel(AppendArgs a)
+{
+    __shared__ uint32_t wsum[16];
+    __shared__ uint32_t base_s;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    if (threadIdx.x == 0) base_s = *a.pool_count;
+    __syncthreads();
+    for (uint32_t b0 = 0; b0 < a.n; b0 += blockDim.x) {
+        uint32_t t = b0 + threadIdx.x;
+        bool keep = t < a.n && a.conf[t] == 0;
+        uint64_t mk = __ballot(keep);
+        if (lane == 0) wsum[w] = __popcll(mk);
+        __syncthreads();
+        uint32_t off = base_s;
+        for (int i = 0; i < w; ++i) off += wsum[i];
+        if (keep) a.pool[off + lanes_below(mk)] = a.in[t];
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t tot = 0;
+            for (int i = 0; i < nw; ++i) tot += wsum[i];
+            base_s += tot;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *a.pool_count = base_s;
+}
+
 __global__ void init_kernel(InitArgs a)
 {
     const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -690,7 +720,8 @@ __global__ void init_kernel(InitArgs a)
     if (i < (size_t)a.n_counters) a.counters[i] = 0;
     if (i == 0) {
         a.n_active[0] = (uint32_t)a.nq;
-        for (int p = 1; p <= a.n_phases; ++p) a.n_active[p] = 0;
+        // later phases' counts and the BOA+ pool counts
+        for (int p = 1; p < 2 * (BOA_MAX_PHASES + 1); ++p) a.n_active[p] = 0;
         *a.status = 0;
     }
 }
@@ -756,6 +787,12 @@ int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds)
 hipError_t launch_compact(const CompactArgs &a, hipStream_t st)
 {
     hipLaunchKernelGGL(compact_kernel, dim3(1), dim3(1024), 0, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_append(const AppendArgs &a, hipStream_t st)
+{
+    hipLaunchKernelGGL(append_kernel, dim3(1), dim3(1024), 0, st, a);
     return hipGetLastError();
 }
 

@@ -72,6 +72,23 @@ def test_tiny_adaptive(tiny, fused):
             (rp["active"], rp["confident"], rp["expansions"], rp["scored"])
 
 
+@pytest.mark.parametrize("sub", [1, 3, 10, 100])
+def test_tiny_boa_plus(tiny, sub):
+    """BOA+ (sub-batched first phase, pooled escalation on a second stream)
+    settles every query exactly as BOA does (Sec. III-A)."""
+    wl, d = tiny["wl"], tiny["data"]
+    sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
+    ref = oracle.boa(tiny["orc"], d.queries, d.ranges, wl.k, sched, eps=0.02)
+    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax, eps=0.02,
+                     boa_plus=True, sub_batches=sub)
+    assert_parity(got, ref, f"BOA+ sub_batches={sub}")
+    st = tiny["gpu"].stats()
+    for p, rp in zip(st["phases"], ref.phases):
+        assert (p["active"], p["confident"], p["expansions"], p["scored"]) == \
+            (rp["active"], rp["confident"], rp["expansions"], rp["scored"])
+    assert st["phases"][0]["launches"] == min(sub, d.queries.shape[0])
+
+
 @pytest.mark.parametrize("L", [10, 16, 64, 128, 500])
 def test_tiny_fixed_width(tiny, L):
     wl, d = tiny["wl"], tiny["data"]
@@ -165,6 +182,10 @@ def test_no_queries(tiny):
         tiny["gpu"].search(q, r, k=10, lds_hash_slots=100)
     with pytest.raises(boa.BoaError):
         tiny["gpu"].search(q, r, k=10, tau=0.1, fused=True)
+    with pytest.raises(boa.BoaError):
+        tiny["gpu"].search(q, r, k=10, tau=0.1, boa_plus=True)
+    with pytest.raises(boa.BoaError):
+        tiny["gpu"].search(q, r, k=10, fused=True, boa_plus=True)
 
 
 # ---------------------------------------------------------------------------
@@ -201,6 +222,8 @@ def test_shapes(shape):
     assert_parity(got, ref, f"shape {shape}")
     got = gpu_search(gpu, q, r, k=10, L0=16, Lmax=256, eps=0.1, fused=True)
     assert_parity(got, ref, f"shape {shape} fused")
+    got = gpu_search(gpu, q, r, k=10, L0=16, Lmax=256, eps=0.1, boa_plus=True, sub_batches=4)
+    assert_parity(got, ref, f"shape {shape} BOA+")
     ref = oracle.boa(orc, q, r, 10, [300])
     got = gpu_search(gpu, q, r, k=10, fixed_L=300, lds_hash_slots=2 * 64 if R < 64 else 256)
     assert_parity(got, ref, f"shape {shape} fixed 300 with spill")
