@@ -131,6 +131,8 @@ def main():
     ap.add_argument("--no-fixed", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle timing")
+    ap.add_argument("--modes", default="phased,fused,boa_plus",
+                    help="adaptive modes to time; the fastest is the headline")
     ap.add_argument("--json-out", default="")
     ap.add_argument("--graph-cache", default="", help="npz file: load the graph if present, else save it")
     ap.add_argument("--copy-probe", type=int, default=0,
@@ -217,7 +219,7 @@ def main():
     modes = {}
     mode_kw = {"phased": {}, "fused": {"fused": True},
                "boa_plus": {"boa_plus": True, "sub_batches": wl.sub_batches}}
-    for mode in ("phased", "fused", "boa_plus"):
+    for mode in args.modes.split(","):
         ms_m, st_m, out_m = timed(dict(kw, **mode_kw[mode]), args.steps, args.warmup)
         modes[mode] = (ms_m, st_m, out_m)
         log(f"adaptive ({mode}): {ms_m:.3f} ms/step, {wl.nq / (ms_m / 1e3):,.0f} QPS")
