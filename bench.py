@@ -131,6 +131,7 @@ def main():
     ap.add_argument("--no-fixed", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle timing")
+    ap.add_argument("--lds-slots", type=int, default=0, help="force the LDS visited-table size")
     ap.add_argument("--modes", default="phased,fused,boa_plus",
                     help="adaptive modes to time; the fastest is the headline")
     ap.add_argument("--json-out", default="")
@@ -199,7 +200,7 @@ def main():
     index = boa.Index(data.vectors, data.attrs, types, adj, entry)
     q = torch.from_numpy(data.queries).to(dev)
     r = torch.from_numpy(data.ranges).to(dev)
-    kw = dict(k=wl.k, L0=wl.L0, Lmax=wl.Lmax, alpha=args.alpha, eps=args.eps)
+    kw = dict(k=wl.k, L0=wl.L0, Lmax=wl.Lmax, alpha=args.alpha, eps=args.eps, lds_hash_slots=args.lds_slots)
 
     def timed(search_kw, steps, warmup):
         """warm-up, then `steps` timed searches bracketed by device syncs;

@@ -14,8 +14,8 @@
 //      the squared L2 distance with a 16-lane (float32) or G-lane (uint8)
 //      group per candidate and a butterfly reduction;
 //   5. pack (phi, distance, id) into one 64-bit key, drop keys that cannot
-//      enter the worklist, compact and bitonic-sort the rest over the
-//      smallest power-of-two lane count, and merge them into the sorted
+//      enter the worklist, sort the rest by counting (each key's rank is the
+//      number of survivors below it), and merge them into the sorted
 //      worklist held in LDS: each new key's rank by binary search, its
 //      output slot marked in a bitmap, and the suffix rebuilt backwards in
 //      64-entry chunks where a popcount of the bitmap tells every output
@@ -98,33 +98,19 @@ __device__ __forceinline__ uint32_t upper_bound32(const uint32_t *a, uint32_t n,
     return lo;
 }
 
-__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int m)
+// Cross-lane move inside a 16-lane row by DPP (no LDS round trip):
+// row_shr:J gives lane i the value of lane i-J; lanes whose source falls
+// outside the row receive 0.
+template <int J>
+__device__ __forceinline__ uint32_t from_lane_minus(uint32_t v)
 {
-    uint32_t lo = __shfl_xor((uint32_t)v, m);
-    uint32_t hi = __shfl_xor((uint32_t)(v >> 32), m);
-    return ((uint64_t)hi << 32) | lo;
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x110 + J, 0xF, 0xF, false);
 }
-
-// Ascending bitonic sort of one 64-bit key per lane over lanes [0, W), W a
-// power of two <= 64 (lanes >= W run the same network on their own blocks).
-__device__ __forceinline__ uint64_t wave_sort64(uint64_t key, int lane, uint32_t W)
+template <int J>
+__device__ __forceinline__ float from_lane_minus_f(float v)
 {
-#pragma unroll
-    for (uint32_t k = 2; k <= 64; k <<= 1) {
-        if (k > W) break;
-#pragma unroll
-        for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-            uint64_t o = shfl_xor64(key, (int)j);
-            bool up = (lane & k) == 0;
-            bool lower = (lane & j) == 0;
-            uint64_t mn = key < o ? key : o;
-            uint64_t mx = key < o ? o : key;
-            key = (lower == up) ? mn : mx;
-        }
-    }
-    return key;
+    return __uint_as_float(from_lane_minus<J>(__float_as_uint(v)));
 }
-
 // ---------------------------------------------------------------------------
 // Distance policies. Each lane group computes one candidate's distance per
 // round; rounds are unrolled by RU so that RU rows of loads are in flight.
@@ -180,13 +166,15 @@ struct F32Scorer {
                     float a3 = x[u][t].w - q[t].w;
                     acc = __builtin_fmaf(a3, a3, acc);
                 }
-                // pairwise tree over the 16 partials: p += p+8, p+4, p+2, p+1
-                acc = acc + __shfl_xor(acc, 8);
-                acc = acc + __shfl_xor(acc, 4);
-                acc = acc + __shfl_xor(acc, 2);
-                acc = acc + __shfl_xor(acc, 1);
+                // pairwise tree over the 16 partials (p += p+8, +4, +2, +1),
+                // mirrored onto the row's top lanes: lane 15 ends with the
+                // same sums in the same order (each add is commutative)
+                acc = acc + from_lane_minus_f<8>(acc);
+                acc = acc + from_lane_minus_f<4>(acc);
+                acc = acc + from_lane_minus_f<2>(acc);
+                acc = acc + from_lane_minus_f<1>(acc);
                 int cj = r0 + 4 * u + g;
-                if (p == 0 && cj < c) cd[cj] = acc;
+                if (p == 15 && cj < c) cd[cj] = acc;
             }
         }
     }
@@ -236,10 +224,15 @@ struct U8Scorer {
 #pragma unroll
             for (int u = 0; u < RU; ++u) {
                 int32_t acc = sq4(x[u].x, q.x) + sq4(x[u].y, q.y) + sq4(x[u].z, q.z) + sq4(x[u].w, q.w);
+                // exact integer sum over the group; the group's top lane holds it
 #pragma unroll
-                for (int s = G >> 1; s > 0; s >>= 1) acc += __shfl_xor(acc, s);
+                for (int s = G >> 1; s >= 16; s >>= 1) acc += __shfl_xor(acc, s);
+                if (G >= 16) acc += (int32_t)from_lane_minus<8>((uint32_t)acc);
+                if (G >= 8) acc += (int32_t)from_lane_minus<4>((uint32_t)acc);
+                if (G >= 4) acc += (int32_t)from_lane_minus<2>((uint32_t)acc);
+                if (G >= 2) acc += (int32_t)from_lane_minus<1>((uint32_t)acc);
                 int cj = r0 + PER * u + g;
-                if (p == 0 && cj < c) cd[cj] = (float)acc;
+                if (p == G - 1 && cj < c) cd[cj] = (float)acc;
             }
         }
     }
@@ -474,14 +467,24 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                 const uint64_t keep = __ballot(key != KEY_NONE);
                 const uint32_t kept = __popcll(keep);
                 if (kept > 0) {
-                    // compact the survivors into lanes [0, kept) and sort them
+                    // sort the survivors: each one's rank is the number of
+                    // survivors below it (keys are distinct), read back from
+                    // LDS as broadcasts, two keys per read
                     if (key != KEY_NONE) nkey[lanes_below(keep)] = key;
                     wave_sync();
+                    uint32_t rank = 0;
+                    {
+                        const ulonglong2 *nk2 = reinterpret_cast<const ulonglong2 *>(nkey);
+                        for (uint32_t i = 0; i < kept; i += 2) {
+                            const ulonglong2 pr = nk2[i >> 1];
+                            rank += pr.x < key ? 1u : 0u;
+                            rank += (i + 1 < kept && pr.y < key) ? 1u : 0u;
+                        }
+                    }
+                    wave_sync();
+                    if (key != KEY_NONE) nkey[rank] = key;
+                    wave_sync();
                     key = lane < (int)kept ? nkey[lane] : KEY_NONE;
-                    uint32_t W = 1;
-                    while (W < kept) W <<= 1;
-                    key = wave_sort64(key, lane, W);
-                    if (lane < (int)kept) nkey[lane] = key;
                     // the next node is the smaller of the best new key and the
                     // entry predicted at selection: start its row load now
                     {
