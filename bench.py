@@ -79,7 +79,7 @@ def exact_filtered_topk(torch, X, attrs_t, f32_cols, Q, ranges_t, k, chunk=256):
     return torch.cat(ids_out).cpu().numpy(), torch.cat(d_out).cpu().numpy(), torch.cat(nv_out).cpu().numpy()
 
 
-def recall(ids, dists, gt_ids, gt_d, n_valid, k):
+def recall(ids, dists, gt_ids, gt_d, n_valid, k, per_query=False):
     """strict: |found ∩ GT| / min(k, |D_f|); tie-tolerant: found valid ids
     whose distance does not exceed the k-th exact distance (rel 1e-5)."""
     ids = ids.astype(np.int64)
@@ -96,6 +96,8 @@ def recall(ids, dists, gt_ids, gt_d, n_valid, k):
             tie[i] = min(k, int((fd <= dk * (1 + 1e-5) + 1e-12).sum())) / denom[i]
         else:
             tie[i] = 1.0 if len(f) == 0 else 0.0
+    if per_query:
+        return tie
     return float(strict.mean()), float(tie.mean())
 
 
@@ -136,6 +138,8 @@ def main():
                     help="adaptive modes to time; the fastest is the headline")
     ap.add_argument("--json-out", default="")
     ap.add_argument("--graph-cache", default="", help="npz file: load the graph if present, else save it")
+    ap.add_argument("--vector-graph", action="store_true",
+                    help="build the graph from vector distances only (no attribute-aware edges)")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -172,19 +176,21 @@ def main():
     t = time.time()
     data = gen.generate(wl)
     log(f"generated {wl.name}: n={wl.n} d={wl.d} m={wl.m} nq={wl.nq} in {time.time() - t:.1f}s")
+    types = np.array(wl.attr_dtypes, dtype=np.int32)
     t = time.time()
-    if args.graph_cache and os.path.exists(args.graph_cache):
-        z = np.load(args.graph_cache)
+    recipe = f"{wl.name}/n={wl.n}/" + ("vector" if args.vector_graph else "attribute-aware")
+    z = np.load(args.graph_cache) if args.graph_cache and os.path.exists(args.graph_cache) else None
+    if z is not None and "recipe" in z and str(z["recipe"]) == recipe:
         adj, entry = z["adj"], int(z["entry"])
     else:
-        adj, entry = graph.build_graph(data.vectors, wl.R, device=dev)
+        kw = {} if args.vector_graph else dict(attrs=data.attrs, attr_dtypes=types)
+        adj, entry = graph.build_graph(data.vectors, wl.R, device=dev, **kw)
         if args.graph_cache:
-            np.savez(args.graph_cache, adj=adj, entry=entry)
+            np.savez(args.graph_cache, adj=adj, entry=entry, recipe=recipe)
     deg = float((adj != graph.PAD).sum(1).mean())
-    log(f"graph R={wl.R} (mean degree {deg:.1f}) entry={entry} in {time.time() - t:.1f}s")
+    log(f"graph R={wl.R} ({recipe}, mean degree {deg:.1f}) entry={entry} in {time.time() - t:.1f}s")
     torch.cuda.empty_cache()
 
-    types = np.array(wl.attr_dtypes, dtype=np.int32)
     f32_cols = {j for j, tt in enumerate(wl.attr_dtypes) if tt == gen.ATTR_F32}
     t = time.time()
     Xg = torch.from_numpy(data.vectors).to(dev).float()
@@ -238,7 +244,11 @@ def main():
     L_avg = float(final_L.mean())
     L_work = float(sum(p["L"] * p["active"] for p in st["phases"]) / wl.nq)
     split = {str(p["L"]): round(100.0 * float((final_L == p["L"]).mean()), 2) for p in st["phases"]}
-    log(f"recall@10 {rec_tie:.4f} (strict {rec_strict:.4f}); L_avg {L_avg:.1f}; split {split}")
+    rq = recall(ids, dists, gt_ids, gt_d, n_valid, wl.k, per_query=True)
+    rec_by_L = {str(p["L"]): round(float(rq[final_L == p["L"]].mean()), 4)
+                for p in st["phases"] if (final_L == p["L"]).any()}
+    log(f"recall@10 {rec_tie:.4f} (strict {rec_strict:.4f}); L_avg {L_avg:.1f}; split {split}; "
+        f"recall by final L {rec_by_L}")
 
     # roofline: the search kernel (every launch is the same kernel)
     bytes_step = gathered_bytes(st)
@@ -299,7 +309,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "n": wl.n, "d": wl.d, "R": wl.R, "m": wl.m, "nq": wl.nq,
                    "k": wl.k, "L0": wl.L0, "Lmax": wl.Lmax, "alpha": args.alpha, "eps": args.eps,
-                   "schedule": sched, "mode": f"BOA ({mode} phases)"},
+                   "schedule": sched, "mode": f"BOA ({mode} phases)", "graph": recipe},
         "modes": {m2: {"ms_per_step": round(v[0], 4), "qps": round(wl.nq / (v[0] / 1e3), 1),
                        "launches_per_step": round(v[1]["cum_launches"] / max(1, v[1]["cum_searches"]), 2)}
                   for m2, v in modes.items()},
@@ -308,6 +318,7 @@ def main():
         "L_avg": round(L_avg, 2),
         "L_work": round(L_work, 2),
         "phase_split_pct": split,
+        "recall_by_final_L": rec_by_L,
         "phases": [{k2: (round(v, 4) if isinstance(v, float) else v) for k2, v in p.items()}
                    for p in st["phases"]],
         "fixed_L500": fixed,

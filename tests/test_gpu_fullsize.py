@@ -23,9 +23,10 @@ def _setup(name):
     from workloads import gen, graph
     wl = gen.BY_NAME[name]
     data = gen.generate(wl)
-    adj, entry = graph.build_graph(data.vectors, wl.R, device="cuda:0")
-    torch.cuda.empty_cache()
     types = np.array(wl.attr_dtypes, dtype=np.int32)
+    # the benchmark's graph: vector edges plus attribute-aware edges
+    adj, entry = graph.build_graph(data.vectors, wl.R, device="cuda:0", attrs=data.attrs, attr_dtypes=types)
+    torch.cuda.empty_cache()
     gpu = boa.Index(data.vectors, data.attrs, types, adj, entry)
     orc = oracle.Index(data.vectors, data.attrs, types, adj, entry)
     q = torch.from_numpy(data.queries).to("cuda:0")

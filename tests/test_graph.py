@@ -1,0 +1,83 @@
+"""The offline graph builder's attribute-aware pass (input preparation, not
+the search path): quantile coordinates, the attribute distance, threshold
+candidates against brute force, and the invariants of the assembled rows."""
+import numpy as np
+import pytest
+import torch
+
+from workloads import gen, graph
+
+
+def test_attribute_quantiles_ties_and_float_columns():
+    a = np.array([[5, 0], [1, 0], [5, 0], [9, 0]], dtype=np.int32)
+    a[:, 1] = gen.f32_bits([0.5, -2.0, 3.0, -0.0])
+    q = graph.attribute_quantiles(a, [gen.ATTR_I32, gen.ATTR_F32])
+    # column 0: ranks 2, 1, 2.5 (tie), 4 -> mid-ranks 2.5, 1, 2.5, 4
+    np.testing.assert_allclose(q[:, 0], (np.array([2.5, 1.0, 2.5, 4.0]) - 0.5) / 4)
+    # float column ranked by value (-2 < -0 < 0.5 < 3), not by bit pattern
+    np.testing.assert_allclose(q[:, 1], (np.array([3.0, 1.0, 4.0, 2.0]) - 0.5) / 4)
+
+
+def _small(n=700, d=8, m=2, seed=3):
+    g = np.random.default_rng(seed)
+    x = g.normal(size=(n, d)).astype(np.float32)
+    a = g.integers(0, 50, size=(n, m)).astype(np.int32)
+    return x, a
+
+
+def test_threshold_candidates_match_brute_force():
+    x, a = _small()
+    n = x.shape[0]
+    X = torch.from_numpy(x).double()
+    QA = torch.from_numpy(graph.attribute_quantiles(a, [0, 0]))
+    levels = (0.01, 0.1)
+    thr = graph._thresholds(QA, levels, seed=1, chunk=128)
+    du, cand, du_l, cand_l = graph.candidates(X, 12, QA, thr, 6, chunk=128)
+    xd = x.astype(np.float64)
+    D = ((xd[:, None, :] - xd[None, :, :]) ** 2).sum(-1)
+    np.fill_diagonal(D, np.inf)
+    qa = QA.numpy()
+    A = np.abs(qa[:, None, :] - qa[None, :, :]).max(-1)
+    for i in range(0, n, 37):
+        o = np.lexsort((np.arange(n), D[i]))[:12]
+        assert cand[i].tolist() == o.tolist()
+        for li in range(len(levels)):
+            Dm = np.where(A[i] > thr[i, li].item(), np.inf, D[i])
+            o = np.lexsort((np.arange(n), Dm))[:6]
+            fin = np.isfinite(Dm[o])
+            got_d = du_l[li, i].numpy()
+            assert np.array_equal(np.isfinite(got_d), fin)
+            assert cand_l[li, i][torch.from_numpy(fin)].tolist() == o[fin].tolist()
+            # every finite candidate lies within the point's threshold
+            assert (A[i][cand_l[li, i][torch.from_numpy(fin)].numpy()] <= thr[i, li].item()).all()
+
+
+def test_attribute_graph_rows_are_valid_and_reachable():
+    x, a = _small(n=1500, d=16)
+    R = 16
+    adj, entry = graph.build_graph(x, R, "cpu", attrs=a, attr_dtypes=[0, 0])
+    n = x.shape[0]
+    assert adj.shape == (n, R) and adj.dtype == np.uint32
+    for i in range(n):
+        row = adj[i][adj[i] != graph.PAD].astype(np.int64)
+        assert i not in row
+        assert len(set(row.tolist())) == len(row)
+        assert (row < n).all()
+    assert graph._reachable(n, adj, entry).all()
+
+
+def test_attribute_edges_raise_valid_neighbour_share():
+    # points whose attributes are close should link to each other more often
+    # than the vector-only graph links them
+    x, a = _small(n=1500, d=16, m=1, seed=5)
+    R = 16
+    adj_v, _ = graph.build_graph(x, R, "cpu")
+    adj_a, _ = graph.build_graph(x, R, "cpu", attrs=a, attr_dtypes=[0])
+
+    def near_share(adj):
+        src = np.repeat(np.arange(len(adj)), R)
+        dst = adj.reshape(-1)
+        ok = dst != graph.PAD
+        return float((np.abs(a[src[ok], 0] - a[dst[ok].astype(np.int64), 0]) <= 1).mean())
+
+    assert near_share(adj_a) > near_share(adj_v) + 0.05

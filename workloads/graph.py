@@ -18,6 +18,16 @@ and it is deliberately not the paper's builder:
   4. connectivity repair: every point is made reachable from the entry
      point (the point nearest the data centroid).
 
+With attributes given, rows also carry attribute-aware edges in the manner
+of JAG's threshold pruning (Sec. II "Graph construction"): each attribute
+value is mapped to its quantile in its column, the attribute distance of
+two points is the largest quantile gap over the columns, and for each of a
+few thresholds t (per-point quantiles of the attribute distance to a
+seeded sample) a point links, under its own degree budget, to the
+alpha-pruned nearest vectors among the points within attribute distance t.
+Under a narrow range predicate the valid points then keep edges among
+themselves, which a valid-first search needs.
+
 Rows are fixed-width n x R uint32 with 0xFFFFFFFF padding. Everything is
 deterministic for a given device. Distances here are this module's own
 (float64 on the CPU, float32 GEMM on a GPU) and share no code with either
@@ -201,26 +211,133 @@ def _reachable(n: int, adj: np.ndarray, s: int) -> np.ndarray:
     return seen
 
 
+def attribute_quantiles(attrs: np.ndarray, attr_dtypes) -> np.ndarray:
+    """n x m float64: each cell's mid-rank in its column divided by n (ties
+    share one value); float32 columns are ranked by value, not by bits."""
+    from scipy.stats import rankdata
+    n, m = attrs.shape
+    out = np.empty((n, m), dtype=np.float64)
+    for j in range(m):
+        col = attrs[:, j]
+        if int(attr_dtypes[j]) == 1:
+            col = np.ascontiguousarray(col).view(np.float32)
+        out[:, j] = (rankdata(col, method="average") - 0.5) / n
+    return out
+
+
+def _attr_dist(A: torch.Tensor, B: torch.Tensor) -> torch.Tensor:
+    """Largest per-column quantile gap between rows of A and rows of B."""
+    d = None
+    for j in range(A.shape[1]):
+        g = (A[:, j:j + 1] - B[None, :, j]).abs()
+        d = g if d is None else torch.maximum(d, g)
+    return d
+
+
+def _thresholds(QA: torch.Tensor, levels, seed: int, chunk: int) -> torch.Tensor:
+    """n x len(levels): per point, the given quantiles of its attribute
+    distance to a seeded sample of points."""
+    n = QA.shape[0]
+    dev = QA.device
+    g = np.random.Generator(np.random.PCG64(seed ^ 0x5A5A))
+    S = min(n - 1, 4096)
+    samp = torch.from_numpy(np.sort(g.choice(n, size=S, replace=False))).to(dev)
+    thr = torch.empty((n, len(levels)), dtype=QA.dtype, device=dev)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        ds, _ = torch.sort(_attr_dist(QA[s:e], QA[samp]), dim=1)
+        for li, lv in enumerate(levels):
+            thr[s:e, li] = ds[:, min(S - 1, int(lv * S))]
+    return thr
+
+
+def candidates(X: torch.Tensor, K: int, QA: torch.Tensor | None = None, thr: torch.Tensor | None = None,
+               K_attr: int = 0, chunk: int = 2048):
+    """One exhaustive pass: every point's K nearest others (dist, ids) and,
+    with attribute quantiles QA and thresholds thr (n x levels), its K_attr
+    nearest among the points within each threshold (levels x n x K_attr,
+    missing = inf / unspecified id). Sorted by (distance, id)."""
+    n = X.shape[0]
+    dev = X.device
+    nx = (X * X).sum(1)
+    kk = min(n, K + 5)
+    du = torch.empty((n, K), dtype=X.dtype, device=dev)
+    cand = torch.empty((n, K), dtype=torch.int64, device=dev)
+    nl = 0 if thr is None else thr.shape[1]
+    ka = min(n, K_attr + 5)
+    du_l = torch.empty((nl, n, K_attr), dtype=X.dtype, device=dev)
+    cand_l = torch.empty((nl, n, K_attr), dtype=torch.int64, device=dev)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        D = _sq_dist(X[s:e], X, nx[s:e], nx)
+        r = torch.arange(s, e, device=dev)
+        D[r - s, r] = float("inf")
+        dv, di = torch.topk(D, kk, dim=1, largest=False, sorted=True)
+        dv, di = _sort_by_dist_then_id(dv, di)
+        du[s:e], cand[s:e] = dv[:, :K], di[:, :K]
+        if nl:
+            A = _attr_dist(QA[s:e], QA)
+            for li in range(nl):
+                Dl = torch.where(A > thr[s:e, li:li + 1], torch.full_like(D, float("inf")), D)
+                dv, di = torch.topk(Dl, ka, dim=1, largest=False, sorted=True)
+                dv, di = _sort_by_dist_then_id(dv, di)
+                du_l[li, s:e], cand_l[li, s:e] = dv[:, :K_attr], di[:, :K_attr]
+                del Dl
+            del A
+        del D
+    return du, cand, du_l, cand_l
+
+
+def attribute_edges(X: torch.Tensor, du_l: torch.Tensor, cand_l: torch.Tensor, budget: int,
+                    alpha: float) -> torch.Tensor:
+    """n x (levels * budget) ids (-1 = none): per threshold level, the
+    alpha-pruned nearest vectors among the points within that threshold."""
+    n = X.shape[0]
+    out = []
+    for li in range(du_l.shape[0]):
+        keep = alpha_prune(X, cand_l[li], du_l[li], torch.isfinite(du_l[li]),
+                           torch.full((n,), budget, dtype=torch.int64, device=X.device), alpha)
+        out.append(_compact(torch.where(keep, cand_l[li], torch.full_like(cand_l[li], -1)), budget))
+    return torch.cat(out, 1)
+
+
 def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
-                alpha: float = 1.2, seed: int = 0x9A9A, entry: int | None = None):
-    """Fixed-degree proximity graph; returns (adjacency n x R uint32, entry id)."""
+                alpha: float = 1.2, seed: int = 0x9A9A, entry: int | None = None,
+                attrs: np.ndarray | None = None, attr_dtypes=None,
+                attr_levels=(0.002, 0.02, 0.1), attr_budget: int | None = None,
+                cross_links: int | None = None):
+    """Fixed-degree proximity graph; returns (adjacency n x R uint32, entry id).
+    With `attrs` (n x m cells, column types `attr_dtypes`) rows also hold
+    attribute-aware edges, `attr_budget` (default R // 8) per threshold level."""
     dev = torch.device(device)
     n = vectors.shape[0]
     s_id = entry_point(vectors) if entry is None else int(entry)
     X = _as_float(vectors, dev)
     Kc = min(2 * R, n - 1)
-
-    # 1-2: exact kNN candidates, pruned.
+    # 1-2: exact kNN candidates (and, with attributes, the attribute-aware
+    # candidates of every threshold level from the same distance pass).
     t0 = time.time()
-    du, cand = knn(X, Kc)
-    _log(f"exact {Kc}-NN of {n} points in {time.time() - t0:.1f}s")
-    R_cross = max(2, R // 4)
+    attr_e = None
+    if attrs is not None and len(attr_levels) > 0:
+        QA = _as_float(attribute_quantiles(attrs, attr_dtypes), dev)
+        b = max(1, R // 8) if attr_budget is None else int(attr_budget)
+        thr = _thresholds(QA, attr_levels, seed, 2048)
+        du, cand, du_l, cand_l = candidates(X, Kc, QA, thr, min(n - 1, 2 * b))
+        attr_e = attribute_edges(X, du_l, cand_l, b, alpha)
+        del du_l, cand_l, QA, thr
+        _log(f"exact {Kc}-NN and attribute-aware edges ({len(attr_levels)} levels x {b}) "
+             f"of {n} points in {time.time() - t0:.1f}s")
+    else:
+        du, cand, _, _ = candidates(X, Kc)
+        _log(f"exact {Kc}-NN of {n} points in {time.time() - t0:.1f}s")
+    R_cross = max(2, R // 4) if cross_links is None else int(cross_links)
     R_long = R_cross + 1
     K_nav = max(2, R // 2)
 
     # reverse edges (NSG/Vamana style): every kept edge u->v offers u to v.
     reserve = 1 if R >= 8 else 0   # one free slot per row for the connectivity repair
-    base_budget = torch.full((n,), R - R_long - reserve, dtype=torch.int64, device=dev)
+    n_attr = 0 if attr_e is None else attr_e.shape[1]
+    base_budget = torch.full((n,), max(1, R - R_long - reserve - n_attr), dtype=torch.int64, device=dev)
     keep0 = alpha_prune(X, cand, du, torch.ones_like(cand, dtype=torch.bool), base_budget, alpha)
     cand, du = _with_reverse(cand, du, keep0, Kc)
     rows0 = torch.where(torch.isfinite(du), cand, torch.full_like(cand, -1)).cpu().numpy()
@@ -270,11 +387,14 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
     near = torch.cat([cross, own], 1)
     _log(f"navigation: {len(P)} sample points, {R_cross} cross-component links per point")
 
-    long = torch.cat([nav_links, near], 1)
+    long = torch.cat([nav_links, near] + ([] if attr_e is None else [attr_e]), 1)
     dup = torch.zeros_like(long, dtype=torch.bool)
     for j in range(1, long.shape[1]):
         dup[:, j] = (long[:, :j] == long[:, j:j + 1]).any(1)
-    long = _compact(torch.where(dup, torch.full_like(long, -1), long), long.shape[1])
+    self_l = long == torch.arange(n, device=dev)[:, None]
+    long = _compact(torch.where(dup | self_l, torch.full_like(long, -1), long), long.shape[1])
+    if long.shape[1] > R - reserve:
+        long[:, R - reserve:] = -1
     n_long = (long >= 0).sum(1)
 
     # base candidates not already linked, pruned into the remaining budget.
