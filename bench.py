@@ -119,6 +119,10 @@ def gathered_bytes(stats) -> float:
     return float(sum(p["gathered_bytes"] for p in stats["phases"]))
 
 
+def gathered_bytes_phase(stats, i: int) -> float:
+    return float(stats["phases"][i]["gathered_bytes"])
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -128,13 +132,15 @@ def main():
     ap.add_argument("--n", type=int, default=0, help="scale the workload down to n points (testing)")
     ap.add_argument("--nq", type=int, default=0)
     ap.add_argument("--eps", type=float, default=0.05)
+    ap.add_argument("--alt-alpha", type=float, default=32.0,
+                    help="also time the headline mode with this growth factor (0: skip)")
     ap.add_argument("--alpha", type=float, default=2.0)
     ap.add_argument("--fixed-steps", type=int, default=3)
     ap.add_argument("--no-fixed", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle timing")
     ap.add_argument("--lds-slots", type=int, default=0, help="force the LDS visited-table size")
-    ap.add_argument("--modes", default="phased,fused,boa_plus",
+    ap.add_argument("--modes", default="phased,fused,split,boa_plus",
                     help="adaptive modes to time; the fastest is the headline")
     ap.add_argument("--json-out", default="")
     ap.add_argument("--graph-cache", default="", help="npz file: load the graph if present, else save it")
@@ -224,7 +230,7 @@ def main():
         return (t1 - t0) * 1e3 / steps, index.stats(), o
 
     modes = {}
-    mode_kw = {"phased": {}, "fused": {"fused": True},
+    mode_kw = {"phased": {}, "fused": {"fused": True}, "split": {"split": True},
                "boa_plus": {"boa_plus": True, "sub_batches": wl.sub_batches}}
     for mode in args.modes.split(","):
         ms_m, st_m, out_m = timed(dict(kw, **mode_kw[mode]), args.steps, args.warmup)
@@ -250,15 +256,46 @@ def main():
     log(f"recall@10 {rec_tie:.4f} (strict {rec_strict:.4f}); L_avg {L_avg:.1f}; split {split}; "
         f"recall by final L {rec_by_L}")
 
-    # roofline: the search kernel (every launch is the same kernel)
-    bytes_step = gathered_bytes(st)
-    launches_step = st["cum_launches"] / max(1, st["cum_searches"])
-    avg_launch_ms = st["cum_kernel_ms"] / max(1, st["cum_launches"])
-    bytes_launch = bytes_step / launches_step
-    achieved = bytes_launch / (avg_launch_ms * 1e-3) / 1e9
+    # roofline of the dominant kernel: launches are grouped by the phase they
+    # start at (a split search has two kernels: the first phase, and the
+    # escalation through every later phase); each group's algorithmic bytes
+    # are the gathered bytes of the phases its launches cover
+    nph = len(st["phases"])
+    starts = [i for i in range(nph) if st["cum_phase_launches"][i] > 0]
+    groups = []
+    for gi, i in enumerate(starts):
+        j = starts[gi + 1] if gi + 1 < len(starts) else nph
+        if mode == "fused":
+            j = nph
+        nl = st["cum_phase_launches"][i]
+        kms = st["cum_phase_kernel_ms"][i] / nl
+        b = sum(gathered_bytes_phase(st, q) for q in range(i, j)) * args.steps / nl
+        groups.append(dict(phases=f"{st['phases'][i]['L']}..{st['phases'][j - 1]['L']}", launches=nl,
+                           avg_launch_ms=round(kms, 5), bytes_per_launch=round(b),
+                           GBps=round(b / (kms * 1e-3) / 1e9, 1),
+                           time_share=round(st["cum_phase_kernel_ms"][i] / st["cum_kernel_ms"], 4)))
+    dom = max(groups, key=lambda g: g["time_share"])
+    bytes_launch, avg_launch_ms = dom["bytes_per_launch"], dom["avg_launch_ms"]
+    achieved = dom["GBps"]
     kernel_share = st["cum_kernel_ms"] / (ms * args.steps)
-    log(f"kernel ({mode}): {avg_launch_ms:.4f} ms/launch avg over {st['cum_launches']} launches, "
-        f"{bytes_launch / 1e6:.2f} MB/launch -> {achieved:.1f} GB/s; kernel time share {kernel_share:.2f}")
+    log(f"kernel ({mode}): dominant launch group {dom['phases']}: {avg_launch_ms:.4f} ms/launch avg over "
+        f"{dom['launches']} launches, {bytes_launch / 1e6:.2f} MB/launch -> {achieved:.1f} GB/s; "
+        f"kernel time share {kernel_share:.2f}; groups {groups}")
+
+    variant = None
+    if args.alt_alpha > 0:
+        kv = dict(kw, alpha=args.alt_alpha, **mode_kw[mode])
+        msv, stv, out_v = timed(kv, args.steps, args.warmup)
+        fl_v = out_v.final_L.cpu().numpy()
+        ids_v = out_v.ids.cpu().numpy().view(np.uint32)
+        rq_v = recall(ids_v, out_v.dists.cpu().numpy(), gt_ids, gt_d, n_valid, wl.k, per_query=True)
+        variant = dict(alpha=args.alt_alpha, schedule=[p["L"] for p in stv["phases"]], mode=mode,
+                       ms_per_step=round(msv, 4), qps=round(wl.nq / (msv / 1e3), 1),
+                       recall_at_10=round(float(rq_v.mean()), 5), L_avg=round(float(fl_v.mean()), 2),
+                       recall_by_final_L={str(p["L"]): round(float(rq_v[fl_v == p["L"]].mean()), 4)
+                                          for p in stv["phases"] if (fl_v == p["L"]).any()})
+        log(f"schedule variant alpha={args.alt_alpha} ({mode}): {msv:.3f} ms/step, "
+            f"{variant['qps']:,.0f} QPS, recall {variant['recall_at_10']:.4f}, L_avg {variant['L_avg']:.1f}")
 
     fixed = None
     if not args.no_fixed:
@@ -321,12 +358,16 @@ def main():
         "recall_by_final_L": rec_by_L,
         "phases": [{k2: (round(v, 4) if isinstance(v, float) else v) for k2, v in p.items()}
                    for p in st["phases"]],
+        "schedule_variant": variant,
         "fixed_L500": fixed,
         "speedup_vs_fixed_L500": round(qps / fixed["qps"], 3) if fixed else None,
-        "roofline": {"bound": "hbm", "kernel": KERNEL, "mode": mode, "achieved": round(achieved, 1),
+        "roofline": {"bound": "hbm", "kernel": KERNEL, "mode": mode, "phases": dom["phases"],
+                     "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": recorded_traffic(f"{wl.name}/{mode}"), "bytes_per_launch": round(bytes_launch),
-                     "avg_launch_ms": round(avg_launch_ms, 5), "launches": st["cum_launches"]},
+                     "traffic": recorded_traffic(f"{wl.name}/{mode}/{dom['phases']}"),
+                     "bytes_per_launch": round(bytes_launch),
+                     "avg_launch_ms": round(avg_launch_ms, 5), "launches": dom["launches"],
+                     "launch_groups": groups},
         "cpu_baseline": cpu,
     }
     line = json.dumps(res)

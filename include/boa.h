@@ -110,8 +110,14 @@ typedef struct {
     int32_t fused;          /* 1: run every phase in one persistent launch, each wave
                                carrying its query from width to width without waiting
                                for the other queries (identical results, since every
-                               phase restarts the search; needs tau == 0). 0: one launch
-                               per phase with device-side compaction between them. */
+                               phase restarts the search; needs tau == 0). 2: split:
+                               the first phase in one launch, then (after compaction
+                               and a 4-byte read of the survivor count) every later
+                               phase in one persistent launch over the survivors, whose
+                               waves get the largest visited table that still lets all
+                               survivors run at once (identical results; needs
+                               tau == 0). 0: one launch per phase with device-side
+                               compaction between them. */
 } boa_params;
 
 void boa_default_params(boa_params *p);
@@ -160,6 +166,10 @@ typedef struct {
     int64_t cum_searches, cum_launches;
     double cum_kernel_ms;
     boa_phase_stats phase[BOA_MAX_PHASES];
+    /* accumulated like cum_*, split by the phase a launch starts at (a fused
+       launch counts under phase 0, a split search's second launch under 1) */
+    int64_t cum_phase_launches[BOA_MAX_PHASES];
+    double cum_phase_kernel_ms[BOA_MAX_PHASES];
 } boa_stats;
 
 /* Statistics of the last search (per phase) plus the accumulated counters.

@@ -51,7 +51,8 @@ class Stats(C.Structure):
     _fields_ = [("n_phases", C.c_int32), ("waves_per_block", C.c_int32), ("blocks", C.c_int32),
                 ("lds_hash_slots", C.c_int32), ("spilled_queries", C.c_int64), ("total_ms", C.c_float),
                 ("cum_searches", C.c_int64), ("cum_launches", C.c_int64), ("cum_kernel_ms", C.c_double),
-                ("phase", PhaseStats * MAX_PHASES)]
+                ("phase", PhaseStats * MAX_PHASES),
+                ("cum_phase_launches", C.c_int64 * MAX_PHASES), ("cum_phase_kernel_ms", C.c_double * MAX_PHASES)]
 
 
 _lib = None
@@ -145,12 +146,14 @@ class Index:
     def search(self, queries, ranges, k: int, L0: int = 16, Lmax: int = 512, alpha: float = 2.0,
                eps: float = 0.05, tau: float = 0.0, fixed_L: int = 0, boa_plus: bool = False,
                sub_batches: int = 10, lds_hash_slots: int = 0, schedule=None, fused: bool = False,
-               counters: bool = False,
+               split: bool = False, counters: bool = False,
                stream=None, out=None) -> SearchResult:
         """Adaptive filtered top-k of a batch of device-resident queries.
 
         queries: torch tensor (nq, d) on the GPU, float32 or uint8 like the index.
         ranges:  torch int32 tensor (nq, m, 2) on the GPU (float32 columns as bit patterns).
+        fused:   every phase in one persistent launch; split: the first phase in
+                 one launch, the survivors through all later phases in a second.
         """
         import torch
         if not (queries.is_cuda and ranges.is_cuda):
@@ -175,7 +178,9 @@ class Index:
         p = default_params()
         p.k, p.L0, p.Lmax, p.alpha, p.eps, p.tau = k, L0, Lmax, alpha, eps, tau
         p.fixed_L, p.boa_plus, p.sub_batches, p.lds_hash_slots = fixed_L, int(boa_plus), sub_batches, lds_hash_slots
-        p.fused = int(fused)
+        if fused and split:
+            raise ValueError("fused and split are exclusive")
+        p.fused = 2 if split else int(fused)
         sched_arr = None
         if schedule is not None:
             sched_arr = (C.c_int32 * len(schedule))(*schedule)
@@ -200,7 +205,9 @@ class Index:
         return dict(phases=phases, waves_per_block=s.waves_per_block, blocks=s.blocks,
                     lds_hash_slots=s.lds_hash_slots, spilled_queries=s.spilled_queries,
                     total_ms=s.total_ms, cum_searches=s.cum_searches, cum_launches=s.cum_launches,
-                    cum_kernel_ms=s.cum_kernel_ms)
+                    cum_kernel_ms=s.cum_kernel_ms,
+                    cum_phase_launches=[int(s.cum_phase_launches[i]) for i in range(s.n_phases)],
+                    cum_phase_kernel_ms=[float(s.cum_phase_kernel_ms[i]) for i in range(s.n_phases)])
 
     def reset_counters(self):
         _check(lib().boa_reset_counters(self._h))

@@ -71,6 +71,8 @@ struct PhasePlan {
     int32_t L;
     int32_t h_slots, wpb, blocks, lds_per_wave;
     int32_t launches;
+    int64_t capacity;   // waves resident at once on the whole GPU
+    bool wide;          // scorer variant with twice the rows in flight
 };
 
 }  // namespace
@@ -113,6 +115,8 @@ struct boa_index {
     bool have_stats = false;
     int64_t cum_searches = 0, cum_launches = 0;
     double cum_kernel_ms = 0.0;
+    int64_t cum_phase_launches[BOA_MAX_PHASES] = {};
+    double cum_phase_kernel_ms[BOA_MAX_PHASES] = {};
 };
 
 extern "C" {
@@ -383,10 +387,11 @@ uint32_t min_table_slots(const boa_index *ix)
     return std::max<uint32_t>(64u, B > 14 ? (8u << (B - 14)) : 64u);
 }
 
-PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t max_active)
+PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t max_active, bool wide = false)
 {
     PhasePlan pl{};
     pl.L = L;
+    pl.wide = wide;
     // visited table: 16-bit slots, 16 per expected scored node of a width-L
     // search, between 1024 and 4096 (2-8 KB); ids that find both of their
     // buckets full go to the HBM bitmap. The table must leave at most 14
@@ -402,7 +407,7 @@ PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t m
     int best_w = 0, best_wpb = 1, best_occ = 1;
     for (int wpb = 4; wpb >= 1; wpb >>= 1) {
         if ((size_t)wpb * pl.lds_per_wave > ix->lds_per_block_max) continue;
-        int occ = phase_occupancy(ix->vec_dtype, ix->view.d, wpb, (size_t)wpb * pl.lds_per_wave);
+        int occ = phase_occupancy(ix->vec_dtype, ix->view.d, wpb, (size_t)wpb * pl.lds_per_wave, wide);
         if (occ * wpb > best_w) {
             best_w = occ * wpb;
             best_wpb = wpb;
@@ -411,11 +416,55 @@ PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t m
     }
     pl.wpb = best_wpb;
     int64_t blocks = (int64_t)std::max(best_occ, 1) * ix->num_cu;
+    pl.capacity = best_w > 0 ? blocks * best_wpb : 0;
     int64_t need = (max_active + best_wpb - 1) / best_wpb;
     if (need < 1) need = 1;
     pl.blocks = (int32_t)std::min<int64_t>(blocks, need);
     pl.launches = 0;
     return pl;
+}
+
+#ifdef BOA_STAGE_PROFILE
+// Per-stage cycle counters of one launch (a diagnostic build only).
+int stage_profile_begin(unsigned long long **prof, size_t pn, hipStream_t st)
+{
+    HIP_TRY(hipMalloc(reinterpret_cast<void **>(prof), pn * 8));
+    HIP_TRY(hipMemsetAsync(*prof, 0, pn * 8, st));
+    return BOA_OK;
+}
+
+int stage_profile_end(unsigned long long *prof, size_t pn, int L, int waves, hipStream_t st)
+{
+    std::vector<unsigned long long> h(pn);
+    HIP_TRY(hipMemcpyAsync(h.data(), prof, pn * 8, hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    double tot[BOA_PROF_SLOTS] = {0};
+    for (size_t i = 0; i < pn; ++i) tot[i % BOA_PROF_SLOTS] += (double)h[i];
+    const double ne = tot[10] > 0 ? tot[10] : 1;
+    std::fprintf(stderr,
+                 "[stage-profile] L=%d waves=%d expansions=%.0f cycles/expansion: select %.0f "
+                 "visit %.0f score %.0f sort %.0f rank %.0f rebuild %.0f | spilled %.2f chunks %.2f "
+                 "row-prefetch hit %.2f reissued %.2f\n",
+                 L, waves, tot[10], tot[0] / ne, tot[1] / ne, tot[2] / ne, tot[3] / ne, tot[4] / ne,
+                 tot[5] / ne, tot[6] / ne, tot[7] / ne, tot[8] / ne, tot[9] / ne);
+    (void)hipFree(prof);
+    return BOA_OK;
+}
+#endif
+
+// The escalation launch of a split search: S survivors, all phases after the
+// first. Widest visited table (fewest spills to the HBM bitmap) whose LDS
+// footprint still lets all S waves be resident at once; the default table
+// when even that is not possible.
+PhasePlan plan_escalation(const boa_index *ix, int32_t L, int64_t S, int32_t forced_h)
+{
+    if (forced_h > 0) return plan_phase(ix, L, forced_h, S, true);
+    PhasePlan dflt = plan_phase(ix, L, 0, S, true);
+    for (uint32_t h = 16384; h > (uint32_t)dflt.h_slots; h >>= 1) {
+        PhasePlan pl = plan_phase(ix, L, (int32_t)h, S, true);
+        if (pl.capacity >= S && (size_t)pl.lds_per_wave <= ix->lds_per_block_max) return pl;
+    }
+    return dflt;
 }
 
 }  // namespace
@@ -442,10 +491,12 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     if (p->lds_hash_slots && (uint32_t)p->lds_hash_slots < min_table_slots(ix))
         return fail(BOA_EINVAL, "lds_hash_slots too small for this index's id width");
     const bool plus = p->boa_plus != 0 && p->fixed_L <= 0;
-    const bool fused = p->fused != 0;
-    if (fused && p->tau != 0.0)
+    if (p->fused < 0 || p->fused > 2) return fail(BOA_EINVAL, "fused must be 0, 1 or 2");
+    const bool split = p->fused == 2;
+    const bool fused = p->fused == 1;
+    if (p->fused != 0 && p->tau != 0.0)
         return fail(BOA_EINVAL, "fused phases need tau == 0 (the residual test counts all queries of a phase)");
-    if (fused && plus) return fail(BOA_EINVAL, "fused and boa_plus are exclusive");
+    if (p->fused != 0 && plus) return fail(BOA_EINVAL, "fused and boa_plus are exclusive");
     if (plus && p->tau != 0.0)
         return fail(BOA_EINVAL, "BOA+ needs tau == 0 (the residual test counts all queries of a phase)");
     if (plus && (p->sub_batches < 1 || p->sub_batches > 1024)) return fail(BOA_EINVAL, "sub_batches out of range");
@@ -468,6 +519,16 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
             return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
         slots = std::max<uint64_t>(slots, (uint64_t)pl.blocks * pl.wpb);
         plans.push_back(pl);
+    }
+    if (split && n_phases > 1) {
+        // every grid the escalation launch may take (it has at most nq waves)
+        const PhasePlan d = plan_phase(ix, sched.back(), p->lds_hash_slots, nq, true);
+        slots = std::max<uint64_t>(slots, (uint64_t)d.blocks * d.wpb);
+        if (p->lds_hash_slots <= 0)
+            for (uint32_t h = 16384; h > (uint32_t)d.h_slots; h >>= 1) {
+                const PhasePlan c = plan_phase(ix, sched.back(), (int32_t)h, nq, true);
+                slots = std::max<uint64_t>(slots, (uint64_t)c.blocks * c.wpb);
+            }
     }
     const int32_t sub = plus ? std::min<int32_t>(p->sub_batches, (int32_t)nq) : 1;
     const int32_t n_counters = n_phases * (sub + 1) + 8;
@@ -537,6 +598,83 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
         ix->launch_phase.push_back({0, ev});
         ++ev;
         pl.launches = 1;
+    } else if (split) {
+        // the first phase over every query at its own width ...
+        PhasePlan &p0 = plans[0];
+        PhaseArgs a = base;
+        a.active = ix->active[0];
+        a.n_active = ix->n_active;
+        a.t_begin = 0;
+        a.t_end = 0xFFFFFFFFu;
+        a.queue = ix->counters;
+        a.p_begin = 0;
+        a.p_end = 1;
+        a.write_conf = 1;
+        a.L_alloc = sched[0];
+        a.h_log2 = ilog2((uint32_t)p0.h_slots);
+        a.lds_per_wave = p0.lds_per_wave;
+        a.waves_per_block = p0.wpb;
+        a.slot_base = 0;
+        HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
+        HIP_TRY(launch_phase(a, ix->vec_dtype, p0.blocks, st));
+        HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
+        ix->launch_phase.push_back({0, ev});
+        ++ev;
+        p0.launches = 1;
+        if (n_phases > 1) {
+            // ... then its survivors, compacted, through every later width
+            CompactArgs ca{};
+            ca.in = ix->active[0];
+            ca.n_in = ix->n_active;
+            ca.conf = ix->conf;
+            ca.out = ix->active[1];
+            ca.n_out = ix->n_active + 1;
+            ca.tau_count = tau_count;
+            HIP_TRY(launch_compact(ca, st));
+            uint32_t S = 0;
+            HIP_TRY(hipMemcpyAsync(&S, ix->n_active + 1, sizeof(S), hipMemcpyDeviceToHost, st));
+            HIP_TRY(hipStreamSynchronize(st));
+            if (S > 0) {
+                PhasePlan pe = plan_escalation(ix, sched.back(), S, p->lds_hash_slots);
+                if ((size_t)pe.lds_per_wave > ix->lds_per_block_max)
+                    return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
+                if ((uint64_t)pe.blocks * pe.wpb > slots)
+                    return fail(BOA_EINVAL, "internal: escalation grid exceeds the spill bitmaps");
+                PhaseArgs e = base;
+                e.active = ix->active[1];
+                e.n_active = ix->n_active + 1;
+                e.t_begin = 0;
+                e.t_end = 0xFFFFFFFFu;
+                e.queue = ix->counters + 1;
+                e.p_begin = 1;
+                e.p_end = n_phases;
+                e.L_alloc = sched.back();
+                e.h_log2 = ilog2((uint32_t)pe.h_slots);
+                e.lds_per_wave = pe.lds_per_wave;
+                e.waves_per_block = pe.wpb;
+                e.slot_base = 0;
+#ifdef BOA_STAGE_PROFILE
+                unsigned long long *prof = nullptr;
+                const size_t pn = (size_t)pe.blocks * pe.wpb * BOA_PROF_SLOTS;
+                if (int rc2 = stage_profile_begin(&prof, pn, st)) return rc2;
+                e.prof = prof;
+#endif
+                HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
+                HIP_TRY(launch_phase(e, ix->vec_dtype, pe.blocks, st, true));
+                HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
+#ifdef BOA_STAGE_PROFILE
+                std::fprintf(stderr, "[stage-profile] split escalation: %u survivors, table %d slots, %d waves\n",
+                             S, pe.h_slots, pe.blocks * pe.wpb);
+                if (int rc2 = stage_profile_end(prof, pn, sched.back(), pe.blocks * pe.wpb, st)) return rc2;
+#endif
+                ix->launch_phase.push_back({1, ev});
+                ++ev;
+                plans[1].launches = 1;
+                plans[1].h_slots = pe.h_slots;
+                plans[1].wpb = pe.wpb;
+                plans[1].blocks = pe.blocks;
+            }
+        }
     } else if (!plus) {
         for (int32_t ph = 0; ph < n_phases; ++ph) {
             PhasePlan &pl = plans[ph];
@@ -557,29 +695,14 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
 #ifdef BOA_STAGE_PROFILE
             unsigned long long *prof = nullptr;
             const size_t pn = (size_t)pl.blocks * pl.wpb * BOA_PROF_SLOTS;
-            HIP_TRY(hipMalloc(reinterpret_cast<void **>(&prof), pn * 8));
-            HIP_TRY(hipMemsetAsync(prof, 0, pn * 8, st));
+            if (int rc2 = stage_profile_begin(&prof, pn, st)) return rc2;
             a.prof = prof;
 #endif
             HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
             HIP_TRY(launch_phase(a, ix->vec_dtype, pl.blocks, st));
             HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
 #ifdef BOA_STAGE_PROFILE
-            {
-                std::vector<unsigned long long> h(pn);
-                HIP_TRY(hipMemcpyAsync(h.data(), prof, pn * 8, hipMemcpyDeviceToHost, st));
-                HIP_TRY(hipStreamSynchronize(st));
-                double tot[BOA_PROF_SLOTS] = {0};
-                for (size_t i = 0; i < pn; ++i) tot[i % BOA_PROF_SLOTS] += (double)h[i];
-                const double ne = tot[10] > 0 ? tot[10] : 1;
-                std::fprintf(stderr,
-                             "[stage-profile] L=%d waves=%d expansions=%.0f cycles/expansion: select %.0f "
-                             "visit %.0f score %.0f sort %.0f rank %.0f rebuild %.0f | spilled %.2f chunks %.2f "
-                             "row-prefetch hit %.2f reissued %.2f\n",
-                             pl.L, pl.blocks * pl.wpb, tot[10], tot[0] / ne, tot[1] / ne, tot[2] / ne, tot[3] / ne,
-                             tot[4] / ne, tot[5] / ne, tot[6] / ne, tot[7] / ne, tot[8] / ne, tot[9] / ne);
-                (void)hipFree(prof);
-            }
+            if (int rc2 = stage_profile_end(prof, pn, pl.L, pl.blocks * pl.wpb, st)) return rc2;
 #endif
             ix->launch_phase.push_back({ph, ev});
             ++ev;
@@ -708,6 +831,8 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
         HIP_TRY(hipEventElapsedTime(&ms, ix->ev_start[lp.second], ix->ev_end[lp.second]));
         ix->cum_kernel_ms += ms;
         ix->cum_launches += 1;
+        ix->cum_phase_kernel_ms[lp.first] += ms;
+        ix->cum_phase_launches[lp.first] += 1;
     }
     if (status & BOA_STATUS_OVERFLOW)
         return fail(BOA_EOVERFLOW, "a visited table overflowed; results are not valid");
@@ -759,6 +884,10 @@ extern "C" int boa_get_stats(const boa_index *ix, boa_stats *out)
     out->cum_searches = ix->cum_searches;
     out->cum_launches = ix->cum_launches;
     out->cum_kernel_ms = ix->cum_kernel_ms;
+    for (int i = 0; i < BOA_MAX_PHASES; ++i) {
+        out->cum_phase_launches[i] = ix->cum_phase_launches[i];
+        out->cum_phase_kernel_ms[i] = ix->cum_phase_kernel_ms[i];
+    }
     return BOA_OK;
 }
 
@@ -768,5 +897,9 @@ extern "C" int boa_reset_counters(boa_index *ix)
     ix->cum_searches = 0;
     ix->cum_launches = 0;
     ix->cum_kernel_ms = 0.0;
+    for (int i = 0; i < BOA_MAX_PHASES; ++i) {
+        ix->cum_phase_launches[i] = 0;
+        ix->cum_phase_kernel_ms[i] = 0.0;
+    }
     return BOA_OK;
 }

@@ -86,8 +86,10 @@ struct InitArgs {
     int32_t n_counters;
 };
 
-hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st);
-int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds);
+// wide: the scorer variant with twice the rows in flight (for launches that
+// hold few waves per CU)
+hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st, bool wide = false);
+int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds, bool wide = false);
 hipError_t launch_compact(const CompactArgs &a, hipStream_t st);
 hipError_t launch_append(const AppendArgs &a, hipStream_t st);
 hipError_t launch_init(const InitArgs &a, hipStream_t st);

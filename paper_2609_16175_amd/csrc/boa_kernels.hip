@@ -115,7 +115,10 @@ __device__ __forceinline__ float from_lane_minus_f(float v)
 // Distance policies. Each lane group computes one candidate's distance per
 // round; rounds are unrolled by RU so that RU rows of loads are in flight.
 
-template <int T>
+// W = 2 is the variant for launches that hold few waves per CU (the
+// escalation of a split search): twice the rows in flight per round trip,
+// paid for in registers that such launches do not need for occupancy.
+template <int T, int W = 1>
 struct F32Scorer {
     // lane p = lane & 15 accumulates float4 chunks p, p+16, p+32, ...
     static constexpr int kGroup = 16;
@@ -134,7 +137,10 @@ struct F32Scorer {
 
     __device__ __forceinline__ void score(const void *V, int d, const uint32_t *cid, int c, float *cd, int lane)
     {
-        constexpr int RU = T <= 2 ? 4 : (T <= 4 ? 2 : 1);
+        // rows in flight per round trip: the narrow variant keeps registers
+        // for occupancy; the wide one covers most expansions in one round trip
+        constexpr int RU = W == 1 ? (T <= 2 ? 4 : (T <= 4 ? 2 : 1))
+                                  : (T <= 2 ? 16 : (T <= 4 ? 8 : (T <= 6 ? 4 : (T <= 12 ? 2 : 1))));
         const float *vec = reinterpret_cast<const float *>(V);
         const int g = lane >> 4, p = lane & 15, nch = d >> 2;
         for (int r0 = 0; r0 < c; r0 += 4 * RU) {
@@ -154,6 +160,7 @@ struct F32Scorer {
             }
 #pragma unroll
             for (int u = 0; u < RU; ++u) {
+                if (r0 + 4 * u >= c) break;   // uniform: no candidate left in this round
                 float acc = 0.0f;
 #pragma unroll
                 for (int t = 0; t < T; ++t) {
@@ -180,7 +187,7 @@ struct F32Scorer {
     }
 };
 
-template <int G>
+template <int G, int W = 1>
 struct U8Scorer {
     // lane p = lane % G holds the query's 16-byte chunk p (p < d/16); the
     // exact int32 sum is order-free.
@@ -208,7 +215,7 @@ struct U8Scorer {
     __device__ __forceinline__ void score(const void *V, int d, const uint32_t *cid, int c, float *cd, int lane)
     {
         constexpr int PER = 64 / G;            // candidates per round
-        constexpr int RU = G <= 8 ? 2 : 4;
+        constexpr int RU = W == 1 ? (G <= 8 ? 2 : 4) : (G <= 16 ? G : 16);
         const uint8_t *vec = reinterpret_cast<const uint8_t *>(V);
         const int g = lane / G, p = lane % G, nch = d >> 4;
         for (int r0 = 0; r0 < c; r0 += PER * RU) {
@@ -223,6 +230,7 @@ struct U8Scorer {
             }
 #pragma unroll
             for (int u = 0; u < RU; ++u) {
+                if (r0 + PER * u >= c) break;   // uniform: no candidate left in this round
                 int32_t acc = sq4(x[u].x, q.x) + sq4(x[u].y, q.y) + sq4(x[u].z, q.z) + sq4(x[u].w, q.w);
                 // exact integer sum over the group; the group's top lane holds it
 #pragma unroll
@@ -749,41 +757,47 @@ static int occupancy_t(int wpb, size_t lds)
     return nb;
 }
 
-#define BOA_DISPATCH(VEC, DIM, CALL)                                         \
+#define BOA_DISPATCH_W(VEC, DIM, W, CALL)                                    \
     do {                                                                     \
         if ((VEC) == BOA_VEC_F32) {                                          \
             int T_ = ((DIM) + 63) / 64;                                      \
-            if (T_ <= 1) { using S_ = F32Scorer<1>; CALL; }                  \
-            else if (T_ <= 2) { using S_ = F32Scorer<2>; CALL; }             \
-            else if (T_ <= 3) { using S_ = F32Scorer<3>; CALL; }             \
-            else if (T_ <= 4) { using S_ = F32Scorer<4>; CALL; }             \
-            else if (T_ <= 6) { using S_ = F32Scorer<6>; CALL; }             \
-            else if (T_ <= 8) { using S_ = F32Scorer<8>; CALL; }             \
-            else if (T_ <= 12) { using S_ = F32Scorer<12>; CALL; }           \
-            else { using S_ = F32Scorer<16>; CALL; }                         \
+            if (T_ <= 1) { using S_ = F32Scorer<1, W>; CALL; }               \
+            else if (T_ <= 2) { using S_ = F32Scorer<2, W>; CALL; }          \
+            else if (T_ <= 3) { using S_ = F32Scorer<3, W>; CALL; }          \
+            else if (T_ <= 4) { using S_ = F32Scorer<4, W>; CALL; }          \
+            else if (T_ <= 6) { using S_ = F32Scorer<6, W>; CALL; }          \
+            else if (T_ <= 8) { using S_ = F32Scorer<8, W>; CALL; }          \
+            else if (T_ <= 12) { using S_ = F32Scorer<12, W>; CALL; }        \
+            else { using S_ = F32Scorer<16, W>; CALL; }                      \
         } else {                                                             \
             int G_ = (DIM) / 16;                                             \
-            if (G_ <= 1) { using S_ = U8Scorer<1>; CALL; }                   \
-            else if (G_ <= 2) { using S_ = U8Scorer<2>; CALL; }              \
-            else if (G_ <= 4) { using S_ = U8Scorer<4>; CALL; }              \
-            else if (G_ <= 8) { using S_ = U8Scorer<8>; CALL; }              \
-            else if (G_ <= 16) { using S_ = U8Scorer<16>; CALL; }            \
-            else if (G_ <= 32) { using S_ = U8Scorer<32>; CALL; }            \
-            else { using S_ = U8Scorer<64>; CALL; }                          \
+            if (G_ <= 1) { using S_ = U8Scorer<1, W>; CALL; }                \
+            else if (G_ <= 2) { using S_ = U8Scorer<2, W>; CALL; }           \
+            else if (G_ <= 4) { using S_ = U8Scorer<4, W>; CALL; }           \
+            else if (G_ <= 8) { using S_ = U8Scorer<8, W>; CALL; }           \
+            else if (G_ <= 16) { using S_ = U8Scorer<16, W>; CALL; }         \
+            else if (G_ <= 32) { using S_ = U8Scorer<32, W>; CALL; }         \
+            else { using S_ = U8Scorer<64, W>; CALL; }                       \
         }                                                                    \
     } while (0)
 
-hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st)
+#define BOA_DISPATCH(VEC, DIM, WIDE, CALL)                                   \
+    do {                                                                     \
+        if (WIDE) BOA_DISPATCH_W(VEC, DIM, 2, CALL);                         \
+        else BOA_DISPATCH_W(VEC, DIM, 1, CALL);                              \
+    } while (0)
+
+hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st, bool wide)
 {
     hipError_t e = hipSuccess;
-    BOA_DISPATCH(vec_dtype, a.ix.d, e = launch_phase_t<S_>(a, blocks, st));
+    BOA_DISPATCH(vec_dtype, a.ix.d, wide, e = launch_phase_t<S_>(a, blocks, st));
     return e;
 }
 
-int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds)
+int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds, bool wide)
 {
     int r = 0;
-    BOA_DISPATCH(vec_dtype, d, r = occupancy_t<S_>(wpb, lds));
+    BOA_DISPATCH(vec_dtype, d, wide, r = occupancy_t<S_>(wpb, lds));
     return r;
 }
 

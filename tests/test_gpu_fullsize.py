@@ -61,7 +61,7 @@ def test_full_size_adaptive_sampled(full):
     wl, d, s = full["wl"], full["data"], full["sample"]
     sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
     ref = oracle.boa(full["orc"], d.queries[s], d.ranges[s], wl.k, sched, threads=16)
-    for mode in ({"fused": True}, {}, {"boa_plus": True, "sub_batches": wl.sub_batches}):
+    for mode in ({"fused": True}, {"split": True}, {}, {"boa_plus": True, "sub_batches": wl.sub_batches}):
         out = full["gpu"].search(full["q"], full["r"], k=wl.k, L0=wl.L0, Lmax=wl.Lmax, counters=True, **mode)
         torch.cuda.synchronize()
         _check(_rows(out, s), ref, f"{wl.name} {mode or 'phased'}")

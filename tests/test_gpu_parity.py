@@ -58,13 +58,16 @@ def tiny():
                 gpu=boa.Index(data.vectors, data.attrs, types, adj, entry))
 
 
-@pytest.mark.parametrize("fused", [False, True])
-def test_tiny_adaptive(tiny, fused):
+MODES = {"phased": {}, "fused": {"fused": True}, "split": {"split": True}}
+
+
+@pytest.mark.parametrize("mode", list(MODES))
+def test_tiny_adaptive(tiny, mode):
     wl, d = tiny["wl"], tiny["data"]
     sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
     ref = oracle.boa(tiny["orc"], d.queries, d.ranges, wl.k, sched)
-    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax, fused=fused)
-    assert_parity(got, ref, f"tiny adaptive fused={fused}")
+    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax, **MODES[mode])
+    assert_parity(got, ref, f"tiny adaptive {mode}")
     st = tiny["gpu"].stats()
     assert [p["L"] for p in st["phases"]] == sched
     for p, rp in zip(st["phases"], ref.phases):
@@ -97,29 +100,29 @@ def test_tiny_fixed_width(tiny, L):
     assert_parity(got, ref, f"tiny fixed L={L}")
 
 
-@pytest.mark.parametrize("slots,fused", [(64, False), (256, False), (64, True)])
-def test_forced_spill_changes_nothing(tiny, slots, fused):
+@pytest.mark.parametrize("slots,mode", [(64, "phased"), (256, "phased"), (64, "fused"), (64, "split")])
+def test_forced_spill_changes_nothing(tiny, slots, mode):
     """A tiny LDS visited table sends almost every insert to the HBM bitmap."""
     wl, d = tiny["wl"], tiny["data"]
     sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
     ref = oracle.boa(tiny["orc"], d.queries, d.ranges, wl.k, sched)
     got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax,
-                     lds_hash_slots=slots, fused=fused)
+                     lds_hash_slots=slots, **MODES[mode])
     assert_parity(got, ref, f"spill slots={slots}")
     assert tiny["gpu"].stats()["spilled_queries"] > 0
     # and twice in a row: a wave slot's bitmap is reset by the next query that spills
     got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax,
-                     lds_hash_slots=slots, fused=fused)
+                     lds_hash_slots=slots, **MODES[mode])
     assert_parity(got, ref, f"spill slots={slots}, repeated")
 
 
-@pytest.mark.parametrize("fused", [False, True])
-def test_paper_schedule(tiny, fused):
+@pytest.mark.parametrize("mode", list(MODES))
+def test_paper_schedule(tiny, mode):
     """The paper's experiments use widths 10, 100, 200 (Sec. IV)."""
     wl, d = tiny["wl"], tiny["data"]
     ref = oracle.boa(tiny["orc"], d.queries, d.ranges, 10, [10, 100, 200], eps=0.02)
     got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=10, schedule=[10, 100, 200], eps=0.02,
-                     fused=fused)
+                     **MODES[mode])
     assert_parity(got, ref, "schedule 10/100/200")
     st = tiny["gpu"].stats()
     for p, rp in zip(st["phases"], ref.phases):
@@ -186,6 +189,12 @@ def test_no_queries(tiny):
         tiny["gpu"].search(q, r, k=10, tau=0.1, boa_plus=True)
     with pytest.raises(boa.BoaError):
         tiny["gpu"].search(q, r, k=10, fused=True, boa_plus=True)
+    with pytest.raises(boa.BoaError):
+        tiny["gpu"].search(q, r, k=10, tau=0.1, split=True)
+    with pytest.raises(boa.BoaError):
+        tiny["gpu"].search(q, r, k=10, split=True, boa_plus=True)
+    with pytest.raises(ValueError):
+        tiny["gpu"].search(q, r, k=10, split=True, fused=True)
 
 
 # ---------------------------------------------------------------------------
@@ -222,9 +231,33 @@ def test_shapes(shape):
     assert_parity(got, ref, f"shape {shape}")
     got = gpu_search(gpu, q, r, k=10, L0=16, Lmax=256, eps=0.1, fused=True)
     assert_parity(got, ref, f"shape {shape} fused")
+    got = gpu_search(gpu, q, r, k=10, L0=16, Lmax=256, eps=0.1, split=True)
+    assert_parity(got, ref, f"shape {shape} split")
     got = gpu_search(gpu, q, r, k=10, L0=16, Lmax=256, eps=0.1, boa_plus=True, sub_batches=4)
     assert_parity(got, ref, f"shape {shape} BOA+")
     ref = oracle.boa(orc, q, r, 10, [300])
     got = gpu_search(gpu, q, r, k=10, fixed_L=300, lds_hash_slots=2 * 64 if R < 64 else 256)
     assert_parity(got, ref, f"shape {shape} fixed 300 with spill")
     gpu.close()
+
+
+@pytest.mark.parametrize("eps", [0.0, 1.0])
+def test_split_all_or_no_survivors(tiny, eps):
+    """eps = 0 sends every query with more than k valid entries on to the
+    wider phases (the escalation launch cannot hold them all at once and
+    falls back to the default table); eps = 1 with unconstrained ranges
+    leaves no survivor, so the escalation launch is skipped."""
+    wl, d = tiny["wl"], tiny["data"]
+    r = d.ranges.copy()
+    if eps == 1.0:
+        r[:, :, 0] = np.iinfo(np.int32).min
+        r[:, :, 1] = np.iinfo(np.int32).max
+    sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
+    ref = oracle.boa(tiny["orc"], d.queries, r, wl.k, sched, eps=eps)
+    got = gpu_search(tiny["gpu"], d.queries, r, k=wl.k, L0=wl.L0, Lmax=wl.Lmax, eps=eps, split=True)
+    assert_parity(got, ref, f"split eps={eps}")
+    st = tiny["gpu"].stats()
+    survivors = int((ref.final_L > wl.L0).sum())
+    assert (survivors == 0) == (eps == 1.0)
+    assert st["phases"][0]["launches"] == 1
+    assert st["phases"][1]["launches"] == (1 if survivors else 0)
