@@ -101,14 +101,22 @@ def recall(ids, dists, gt_ids, gt_d, n_valid, k, per_query=False):
     return float(strict.mean()), float(tie.mean())
 
 
+def source_digest() -> str:
+    """sha256 over the search library's sources (kernels and launch planning):
+    a change to either can change the HBM traffic of a launch."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("boa_kernels.hip", "boa_api.hip", "boa_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2609_16175_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
 def recorded_traffic(workload: str):
     """HBM bytes per launch from the committed counter runs, only while the
-    kernel source is the one they measured (else None)."""
-    import hashlib
+    library sources are the ones they measured (else None)."""
     try:
         rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))[workload]
-        src = os.path.join(ROOT, "paper_2609_16175_amd", "csrc", "boa_kernels.hip")
-        if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["kernel_src_sha256"]:
+        if source_digest() != rec["source_sha256"]:
             return None
         return float(rec["traffic_bytes_per_launch"])
     except (OSError, KeyError, ValueError):

@@ -452,6 +452,21 @@ int stage_profile_end(unsigned long long *prof, size_t pn, int L, int waves, hip
 }
 #endif
 
+// A phase's launch: the automatic table of plan_phase, then doubled (up to
+// 16384 slots) while that keeps as many waves resident (registers, not LDS,
+// often bound narrow phases, so a wider table and fewer spills come free).
+PhasePlan plan_phase_widest(const boa_index *ix, int32_t L, int32_t forced_h, int64_t max_active, bool wide = false)
+{
+    PhasePlan best = plan_phase(ix, L, forced_h, max_active, wide);
+    if (forced_h > 0) return best;
+    for (uint32_t h = 2u * (uint32_t)best.h_slots; h <= 16384u; h <<= 1) {
+        PhasePlan pl = plan_phase(ix, L, (int32_t)h, max_active, wide);
+        if ((size_t)pl.lds_per_wave > ix->lds_per_block_max || pl.capacity < best.capacity) break;
+        best = pl;
+    }
+    return best;
+}
+
 // The escalation launch of a split search: S survivors, all phases after the
 // first. Widest visited table (fewest spills to the HBM bitmap) whose LDS
 // footprint still lets all S waves be resident at once; the default table
@@ -513,7 +528,7 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     for (int32_t ph = 0; ph < n_phases; ++ph) {
         // a fused launch, and a BOA+ escalation launch, size LDS for the widest phase
         const bool wide = fused || (plus && ph > 0);
-        PhasePlan pl = plan_phase(ix, wide ? sched.back() : sched[ph], p->lds_hash_slots, nq);
+        PhasePlan pl = plan_phase_widest(ix, wide ? sched.back() : sched[ph], p->lds_hash_slots, nq);
         pl.L = sched[ph];
         if ((size_t)pl.lds_per_wave > ix->lds_per_block_max)
             return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
