@@ -211,7 +211,8 @@ def main():
     Qg = torch.from_numpy(data.queries).to(dev).float()
     Ag = torch.from_numpy(data.attrs).to(dev)
     Rg = torch.from_numpy(data.ranges).to(dev)
-    gt_ids, gt_d, n_valid = exact_filtered_topk(torch, Xg, Ag, f32_cols, Qg, Rg, wl.k)
+    gt_ids, gt_d, n_valid = exact_filtered_topk(torch, Xg, Ag, f32_cols, Qg, Rg, wl.k,
+                                                chunk=max(8, min(256, (1 << 30) // wl.n)))
     del Xg, Qg, Ag
     torch.cuda.empty_cache()
     log(f"exhaustive filtered top-{wl.k} in {time.time() - t:.1f}s; selectivity median "

@@ -1,5 +1,5 @@
 """GPU parity at the workloads' full sizes, in the benchmark's launch
-configuration: the whole 10,000-query batch runs on the GPU (fused, phased
+configuration: the whole 10,000-query batch runs on the GPU (fused, split, phased
 and BOA+ modes, and the fixed-width baseline); a seeded sample of queries is
 recomputed by the CPU oracle one by one and compared row by row. Because a
 query's result does not depend on the rest of the batch (every phase
@@ -24,7 +24,8 @@ def _setup(name):
     wl = gen.BY_NAME[name]
     data = gen.generate(wl)
     types = np.array(wl.attr_dtypes, dtype=np.int32)
-    # the benchmark's graph: vector edges plus attribute-aware edges
+    # the benchmark's graph: vector edges plus attribute-aware edges (from
+    # k-means lists above 2M points: about 4 minutes for u8-10M-d128)
     adj, entry = graph.build_graph(data.vectors, wl.R, device="cuda:0", attrs=data.attrs, attr_dtypes=types)
     torch.cuda.empty_cache()
     gpu = boa.Index(data.vectors, data.attrs, types, adj, entry)
@@ -50,7 +51,8 @@ def _check(got, ref, what):
                            f"oracle {ref.ids[bad[0]]} / {ref.dists[bad[0]]} L {ref.final_L[bad[0]]}")
 
 
-@pytest.fixture(scope="module", params=["sift-like-1M-d128", "deep-like-1M-d96", "dblp-like-1M-d768"])
+@pytest.fixture(scope="module",
+                params=["sift-like-1M-d128", "deep-like-1M-d96", "dblp-like-1M-d768", "u8-10M-d128"])
 def full(request):
     env = _setup(request.param)
     yield env

@@ -81,3 +81,50 @@ def test_attribute_edges_raise_valid_neighbour_share():
         return float((np.abs(a[src[ok], 0] - a[dst[ok].astype(np.int64), 0]) <= 1).mean())
 
     assert near_share(adj_a) > near_share(adj_v) + 0.05
+
+
+def _clustered(n=3000, d=16, k=12, m=2, seed=11):
+    g = np.random.default_rng(seed)
+    c = g.normal(scale=8.0, size=(k, d))
+    x = (c[g.integers(0, k, size=n)] + g.normal(size=(n, d))).astype(np.float32)
+    a = g.integers(0, 100, size=(n, m)).astype(np.int32)
+    return x, a
+
+
+def test_ivf_candidates_with_every_list_probed_are_exact():
+    x, a = _clustered()
+    X = torch.from_numpy(x).double()
+    QA = torch.from_numpy(graph.attribute_quantiles(a, [0, 0]))
+    thr = graph._thresholds(QA, (0.01, 0.1), seed=1, chunk=512)
+    ref = graph.candidates(X, 10, QA, thr, 6, chunk=512)
+    got = graph.candidates_ivf(X, 10, QA, thr, 6, lists=12, nprobe=12, batch_elems=1 << 22)
+    for r, g_ in zip(ref, got):
+        if r.dtype == torch.int64:
+            fin = torch.isfinite(ref[0]) if r.dim() == 2 else torch.isfinite(ref[2])
+            assert torch.equal(torch.where(fin, r, -1), torch.where(fin, g_, -1))
+        else:
+            assert torch.equal(torch.isinf(r), torch.isinf(g_))
+            fin = torch.isfinite(r)
+            assert torch.allclose(r[fin], g_[fin], rtol=1e-12, atol=1e-9)
+
+
+def test_ivf_candidates_probing_few_lists():
+    x, a = _clustered()
+    X = torch.from_numpy(x).double()
+    QA = torch.from_numpy(graph.attribute_quantiles(a, [0, 0]))
+    thr = graph._thresholds(QA, (0.01, 0.1), seed=1, chunk=512)
+    du, cand, _, _ = graph.candidates(X, 10, chunk=512)
+    dg, cg, dl, cl = graph.candidates_ivf(X, 10, QA, thr, 6, lists=12, nprobe=3, batch_elems=1 << 22)
+    # a restricted search: never closer than the exhaustive one, rank by rank
+    assert (dg >= du - 1e-9).all()
+    # well-separated clusters: nearly all true neighbours are found
+    hit = np.mean([len(set(cand[i].tolist()) & set(cg[i].tolist())) / 10 for i in range(len(x))])
+    assert hit > 0.95
+    # attribute candidates lie within each point's threshold, sorted, no self
+    A = (QA[:, None, :] - QA[None, :, :]).abs().max(-1).values
+    for li in range(2):
+        fin = torch.isfinite(dl[li])
+        rows = torch.arange(len(x))[:, None].expand_as(cl[li])
+        assert (A[rows[fin], cl[li][fin]] <= thr[rows[fin], li]).all()
+        assert (cl[li][fin] != rows[fin]).all()
+        assert (dl[li][:, 1:] >= dl[li][:, :-1]).all()

@@ -112,9 +112,12 @@ def knn(X: torch.Tensor, K: int, targets: torch.Tensor | None = None, exclude_se
 
 
 def alpha_prune(X: torch.Tensor, cand: torch.Tensor, du: torch.Tensor, valid: torch.Tensor,
-                budget: torch.Tensor, alpha: float, chunk: int = 8192) -> torch.Tensor:
-    """Greedy diversification of each row's sorted candidates; returns keep mask."""
+                budget: torch.Tensor, alpha: float, chunk: int = 0) -> torch.Tensor:
+    """Greedy diversification of each row's sorted candidates; returns keep mask.
+    Rows are independent; `chunk` only bounds the temporaries."""
     n, K = cand.shape
+    if chunk <= 0:
+        chunk = 8192 if n <= 2_000_000 or X.device.type == "cpu" else 65536
     keep_all = torch.zeros((n, K), dtype=torch.bool, device=X.device)
     a2 = alpha * alpha
     for s in range(0, n, chunk):
@@ -187,8 +190,8 @@ def _compact(a: torch.Tensor, width: int) -> torch.Tensor:
 def _components(n: int, rows: np.ndarray) -> np.ndarray:
     from scipy.sparse import coo_matrix
     from scipy.sparse.csgraph import connected_components
-    src = np.repeat(np.arange(n, dtype=np.int64), rows.shape[1])
-    dst = rows.reshape(-1).astype(np.int64)
+    src = np.repeat(np.arange(n, dtype=np.int32), rows.shape[1])
+    dst = rows.reshape(-1).astype(np.int32)
     ok = dst >= 0
     g = coo_matrix((np.ones(int(ok.sum()), dtype=np.int8), (src[ok], dst[ok])), shape=(n, n)).tocsr()
     _, lab = connected_components(g, directed=False)
@@ -288,6 +291,120 @@ def candidates(X: torch.Tensor, K: int, QA: torch.Tensor | None = None, thr: tor
     return du, cand, du_l, cand_l
 
 
+def _nearest_centroids(X: torch.Tensor, cent: torch.Tensor, k: int, chunk: int = 65536) -> torch.Tensor:
+    """n x k ids of each row's nearest centroids (squared L2, ties by id)."""
+    nc = (cent * cent).sum(1)
+    out = torch.empty((X.shape[0], k), dtype=torch.int64, device=X.device)
+    for s in range(0, X.shape[0], chunk):
+        e = min(X.shape[0], s + chunk)
+        D = nc[None, :] - 2.0 * (X[s:e] @ cent.T)
+        dv, di = torch.topk(D, min(cent.shape[0], k + 4), dim=1, largest=False, sorted=True)
+        dv, di = _sort_by_dist_then_id(dv, di)
+        out[s:e] = di[:, :k]
+    return out
+
+
+def kmeans(X: torch.Tensor, C: int, iters: int = 6, sample: int = 1 << 20, seed: int = 0):
+    """Lloyd's k-means on a seeded sample (centroids start at sample points)."""
+    n = X.shape[0]
+    g = np.random.Generator(np.random.PCG64(seed ^ 0x1F1F))
+    S = min(n, sample)
+    idx = torch.from_numpy(np.sort(g.choice(n, size=S, replace=False))).to(X.device)
+    Xs = X[idx]
+    cent = Xs[torch.from_numpy(np.sort(g.choice(S, size=C, replace=False))).to(X.device)].clone()
+    for _ in range(iters):
+        a = _nearest_centroids(Xs, cent, 1)[:, 0]
+        sums = torch.zeros_like(cent).index_add_(0, a, Xs)
+        cnt = torch.bincount(a, minlength=C)
+        nz = cnt > 0
+        cent[nz] = sums[nz] / cnt[nz, None].to(X.dtype)
+    return cent
+
+
+def candidates_ivf(X: torch.Tensor, K: int, QA: torch.Tensor | None = None, thr: torch.Tensor | None = None,
+                   K_attr: int = 0, lists: int = 0, nprobe: int = 16, seed: int = 0, batch_elems: int = 1 << 28):
+    """The outputs of `candidates`, searched per k-means list instead of
+    exhaustively: the members of each list against the points of its
+    `nprobe` nearest lists (itself included). Exact within that pool."""
+    n, dev = X.shape[0], X.device
+    C = lists if lists > 0 else max(1, int(round(math.sqrt(n))))
+    t0 = time.time()
+    cent = kmeans(X, C, seed=seed)
+    a = _nearest_centroids(X, cent, 1)[:, 0]
+    order = torch.argsort(a, stable=True)
+    cnt = torch.bincount(a, minlength=C)
+    off = torch.zeros(C + 1, dtype=torch.int64, device=dev)
+    off[1:] = torch.cumsum(cnt, 0)
+    probe = _nearest_centroids(cent, cent, min(C, nprobe))        # C x nprobe (itself first)
+    _log(f"ivf: {C} lists (sizes {int(cnt.min())}..{int(cnt.max())}), {probe.shape[1]} probed, "
+         f"{time.time() - t0:.1f}s")
+    nx = (X * X).sum(1)
+    du = torch.full((n, K), float("inf"), dtype=X.dtype, device=dev)
+    cand = torch.full((n, K), -1, dtype=torch.int64, device=dev)
+    nl = 0 if thr is None else thr.shape[1]
+    du_l = torch.full((nl, n, K_attr), float("inf"), dtype=X.dtype, device=dev)
+    cand_l = torch.full((nl, n, K_attr), -1, dtype=torch.int64, device=dev)
+    cnt_h = cnt.cpu().numpy()
+    off_h = off.cpu().numpy()
+    probe_h = probe.cpu().numpy()
+    psize = cnt_h[probe_h].sum(1)
+    c0 = 0
+    while c0 < C:
+        # clusters [c0, c1) padded to the batch's largest list and pool
+        c1, mm, pm = c0, 0, 0
+        while c1 < C:
+            mm2, pm2 = max(mm, int(cnt_h[c1])), max(pm, int(psize[c1]))
+            if c1 > c0 and (c1 - c0 + 1) * mm2 * pm2 > batch_elems:
+                break
+            mm, pm, c1 = mm2, pm2, c1 + 1
+        B = c1 - c0
+        mem = torch.full((B, mm), -1, dtype=torch.int64)
+        pool = torch.full((B, pm), -1, dtype=torch.int64)
+        for b, c in enumerate(range(c0, c1)):
+            mem[b, :cnt_h[c]] = torch.arange(off_h[c], off_h[c + 1])
+            parts = [torch.arange(off_h[q], off_h[q + 1]) for q in probe_h[c]]
+            pp = torch.cat(parts)
+            pool[b, :pp.numel()] = pp
+        mem, pool = mem.to(dev), pool.to(dev)
+        mid = torch.where(mem >= 0, order[mem.clamp_min(0)], torch.full_like(mem, -1))
+        pid = torch.where(pool >= 0, order[pool.clamp_min(0)], torch.full_like(pool, -1))
+        Xm, Xp = X[mid.clamp_min(0)], X[pid.clamp_min(0)]
+        D = nx[mid.clamp_min(0)][:, :, None] + nx[pid.clamp_min(0)][:, None, :] - 2.0 * torch.bmm(
+            Xm, Xp.transpose(1, 2).contiguous())
+        D.clamp_min_(0)
+        bad = (pid < 0)[:, None, :] | (pid[:, None, :] == mid[:, :, None])
+        D.masked_fill_(bad, float("inf"))
+        ok_rows = mid >= 0
+        rows = mid[ok_rows]
+
+        def take(Dm, k_out, dst_d, dst_i):
+            kk = min(Dm.shape[2], k_out + 5)
+            dv, di = torch.topk(Dm, kk, dim=2, largest=False, sorted=True)
+            ids = torch.gather(pid[:, None, :].expand(-1, Dm.shape[1], -1), 2, di)
+            dv, ids = dv[ok_rows], ids[ok_rows]
+            ids = torch.where(torch.isfinite(dv), ids, torch.full_like(ids, n))
+            dv, ids = _sort_by_dist_then_id(dv, ids)
+            ids = torch.where(torch.isfinite(dv), ids, torch.full_like(ids, -1))
+            w = min(k_out, dv.shape[1])
+            dst_d[rows, :w], dst_i[rows, :w] = dv[:, :w], ids[:, :w]
+
+        take(D, K, du, cand)
+        if nl:
+            A = None
+            for j in range(QA.shape[1]):
+                gj = (QA[mid.clamp_min(0), j][:, :, None] - QA[pid.clamp_min(0), j][:, None, :]).abs()
+                A = gj if A is None else torch.maximum(A, gj)
+            th = thr[mid.clamp_min(0)]                      # B x mm x levels
+            for li in range(nl):
+                Dl = torch.where(A > th[:, :, li:li + 1], torch.full_like(D, float("inf")), D)
+                take(Dl, K_attr, du_l[li], cand_l[li])
+                del Dl
+            del A
+        del D, Xm, Xp
+        c0 = c1
+    return du, cand, du_l, cand_l
+
+
 def attribute_edges(X: torch.Tensor, du_l: torch.Tensor, cand_l: torch.Tensor, budget: int,
                     alpha: float) -> torch.Tensor:
     """n x (levels * budget) ids (-1 = none): per threshold level, the
@@ -305,10 +422,12 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
                 alpha: float = 1.2, seed: int = 0x9A9A, entry: int | None = None,
                 attrs: np.ndarray | None = None, attr_dtypes=None,
                 attr_levels=(0.002, 0.02, 0.1), attr_budget: int | None = None,
-                cross_links: int | None = None):
+                cross_links: int | None = None, exact_limit: int = 2_000_000):
     """Fixed-degree proximity graph; returns (adjacency n x R uint32, entry id).
     With `attrs` (n x m cells, column types `attr_dtypes`) rows also hold
-    attribute-aware edges, `attr_budget` (default R // 8) per threshold level."""
+    attribute-aware edges, `attr_budget` (default R // 8) per threshold level.
+    Above `exact_limit` points the candidates come from k-means lists
+    (`candidates_ivf`) instead of an exhaustive pass."""
     dev = torch.device(device)
     n = vectors.shape[0]
     s_id = entry_point(vectors) if entry is None else int(entry)
@@ -321,15 +440,18 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
     if attrs is not None and len(attr_levels) > 0:
         QA = _as_float(attribute_quantiles(attrs, attr_dtypes), dev)
         b = max(1, R // 8) if attr_budget is None else int(attr_budget)
-        thr = _thresholds(QA, attr_levels, seed, 2048)
-        du, cand, du_l, cand_l = candidates(X, Kc, QA, thr, min(n - 1, 2 * b))
+        thr = _thresholds(QA, attr_levels, seed, 2048 if n <= exact_limit or dev.type == "cpu" else 32768)
+        if n > exact_limit:
+            du, cand, du_l, cand_l = candidates_ivf(X, Kc, QA, thr, min(n - 1, 2 * b), seed=seed)
+        else:
+            du, cand, du_l, cand_l = candidates(X, Kc, QA, thr, min(n - 1, 2 * b))
         attr_e = attribute_edges(X, du_l, cand_l, b, alpha)
         del du_l, cand_l, QA, thr
-        _log(f"exact {Kc}-NN and attribute-aware edges ({len(attr_levels)} levels x {b}) "
+        _log(f"{Kc}-NN and attribute-aware candidates ({len(attr_levels)} levels x {b}) "
              f"of {n} points in {time.time() - t0:.1f}s")
     else:
-        du, cand, _, _ = candidates(X, Kc)
-        _log(f"exact {Kc}-NN of {n} points in {time.time() - t0:.1f}s")
+        du, cand, _, _ = candidates_ivf(X, Kc, seed=seed) if n > exact_limit else candidates(X, Kc)
+        _log(f"{Kc}-NN candidates of {n} points in {time.time() - t0:.1f}s")
     R_cross = max(2, R // 4) if cross_links is None else int(cross_links)
     R_long = R_cross + 1
     K_nav = max(2, R // 2)
