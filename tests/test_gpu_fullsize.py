@@ -33,7 +33,7 @@ def _setup(name):
     q = torch.from_numpy(data.queries).to("cuda:0")
     r = torch.from_numpy(data.ranges).to("cuda:0")
     sample = np.sort(np.random.default_rng(7).choice(wl.nq, SAMPLE, replace=False))
-    return dict(wl=wl, data=data, gpu=gpu, orc=orc, q=q, r=r, sample=sample)
+    return dict(wl=wl, data=data, gpu=gpu, orc=orc, q=q, r=r, sample=sample, adj=adj, entry=entry)
 
 
 def _rows(out, sel):
@@ -57,6 +57,16 @@ def full(request):
     env = _setup(request.param)
     yield env
     env["gpu"].close()
+
+
+def test_full_size_index_builds(full):
+    """Graph construction is its own test item (minutes at 10M points): the
+    adjacency is well formed and every point is reachable from the entry."""
+    from workloads import graph
+    wl = full["wl"]
+    adj = full["adj"]
+    assert adj.shape == (wl.n, wl.R)
+    assert graph._reachable(wl.n, adj, full["entry"]).all()
 
 
 def test_full_size_adaptive_sampled(full):

@@ -327,7 +327,7 @@ def candidates_ivf(X: torch.Tensor, K: int, QA: torch.Tensor | None = None, thr:
     exhaustively: the members of each list against the points of its
     `nprobe` nearest lists (itself included). Exact within that pool."""
     n, dev = X.shape[0], X.device
-    C = lists if lists > 0 else max(1, int(round(math.sqrt(n))))
+    C = lists if lists > 0 else max(1, min(16384, n // 1024))
     t0 = time.time()
     cent = kmeans(X, C, seed=seed)
     a = _nearest_centroids(X, cent, 1)[:, 0]
@@ -348,19 +348,21 @@ def candidates_ivf(X: torch.Tensor, K: int, QA: torch.Tensor | None = None, thr:
     off_h = off.cpu().numpy()
     probe_h = probe.cpu().numpy()
     psize = cnt_h[probe_h].sum(1)
+    # lists in order of pool size, so that a batch pads little
+    seq = np.lexsort((np.arange(C), cnt_h, psize))
     c0 = 0
     while c0 < C:
-        # clusters [c0, c1) padded to the batch's largest list and pool
+        # lists seq[c0:c1] padded to the batch's largest list and pool
         c1, mm, pm = c0, 0, 0
         while c1 < C:
-            mm2, pm2 = max(mm, int(cnt_h[c1])), max(pm, int(psize[c1]))
+            mm2, pm2 = max(mm, int(cnt_h[seq[c1]])), max(pm, int(psize[seq[c1]]))
             if c1 > c0 and (c1 - c0 + 1) * mm2 * pm2 > batch_elems:
                 break
             mm, pm, c1 = mm2, pm2, c1 + 1
         B = c1 - c0
         mem = torch.full((B, mm), -1, dtype=torch.int64)
         pool = torch.full((B, pm), -1, dtype=torch.int64)
-        for b, c in enumerate(range(c0, c1)):
+        for b, c in enumerate(seq[c0:c1]):
             mem[b, :cnt_h[c]] = torch.arange(off_h[c], off_h[c + 1])
             parts = [torch.arange(off_h[q], off_h[q + 1]) for q in probe_h[c]]
             pp = torch.cat(parts)
@@ -538,9 +540,49 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
     adj[for_rows >= 0] = for_rows[for_rows >= 0].astype(np.uint32)
 
     # 4: connectivity repair from the entry point.
-    _log(f"assembled rows; {int((~_reachable(n, adj, s_id)).sum())} points unreachable before repair")
-    adj = repair(adj, vectors, s_id, P, cand.cpu().numpy())
+    left = link_unreachable(adj, s_id, candn)
+    _log(f"assembled rows; unreachable points linked in one pass, {left.size} left for the repair")
+    if left.size:
+        adj = repair(adj, vectors, s_id, P, candn)
     return adj, s_id
+
+
+def link_unreachable(adj: np.ndarray, s_id: int, cand: np.ndarray) -> np.ndarray:
+    """Give every point unreachable from s_id an in-edge from a reachable one,
+    all at once: each such point proposes its candidates in distance order
+    (a point's candidates are sorted nearest first); a reachable proposer
+    target with a free (padding) slot accepts the lowest-id proposal of a
+    round. Points left without a link are returned for the slower repair."""
+    n, R = adj.shape
+    seen = _reachable(n, adj, s_id)
+    U = np.flatnonzero(~seen)
+    if U.size == 0:
+        return U
+    free = (adj == PAD)
+    nfree = free.sum(1)
+    first_free = np.where(nfree > 0, np.argmax(free, axis=1), -1)
+    C = cand[U]
+    pending = np.ones(U.size, dtype=bool)
+    for j in range(C.shape[1]):
+        if not pending.any():
+            break
+        w = C[:, j]
+        ok = pending & (w >= 0)
+        ok[ok] = seen[w[ok]] & (nfree[w[ok]] > 0)
+        if not ok.any():
+            continue
+        ui, wi = U[ok], w[ok]
+        o = np.lexsort((ui, wi))               # per target, lowest proposer first
+        ui, wi = ui[o], wi[o]
+        lead = np.ones(wi.size, dtype=bool)
+        lead[1:] = wi[1:] != wi[:-1]
+        ui, wi = ui[lead], wi[lead]
+        adj[wi, first_free[wi]] = ui.astype(np.uint32)
+        nfree[wi] -= 1
+        row = adj[wi] == PAD
+        first_free[wi] = np.where(row.any(1), np.argmax(row, axis=1), -1)
+        pending[np.searchsorted(U, ui)] = False
+    return U[pending]
 
 
 def repair(adj: np.ndarray, vectors: np.ndarray, s_id: int, P: np.ndarray,
