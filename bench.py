@@ -102,12 +102,14 @@ def recall(ids, dists, gt_ids, gt_d, n_valid, k, per_query=False):
 
 
 def source_digest() -> str:
-    """sha256 over the search library's sources (kernels and launch planning):
-    a change to either can change the HBM traffic of a launch."""
+    """sha256 over the search library's sources (kernels and launch planning)
+    and the workload's input generators (data and graph): a change to any of
+    them can change the HBM traffic of a launch."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("boa_kernels.hip", "boa_api.hip", "boa_internal.h"):
-        h.update(open(os.path.join(ROOT, "paper_2609_16175_amd", "csrc", f), "rb").read())
+    for f in ("paper_2609_16175_amd/csrc/boa_kernels.hip", "paper_2609_16175_amd/csrc/boa_api.hip",
+              "paper_2609_16175_amd/csrc/boa_internal.h", "workloads/gen.py", "workloads/graph.py"):
+        h.update(open(os.path.join(ROOT, f), "rb").read())
     return h.hexdigest()
 
 
