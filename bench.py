@@ -141,10 +141,13 @@ def main():
     ap.add_argument("--workload", default="sift-like-1M-d128")
     ap.add_argument("--n", type=int, default=0, help="scale the workload down to n points (testing)")
     ap.add_argument("--nq", type=int, default=0)
-    ap.add_argument("--eps", type=float, default=0.05)
-    ap.add_argument("--alt-alpha", type=float, default=32.0,
-                    help="also time the headline mode with this growth factor (0: skip)")
-    ap.add_argument("--alpha", type=float, default=2.0)
+    ap.add_argument("--eps", type=float, default=0.0,
+                    help="confidence threshold of Eq. 3; 0: choose from --eps-grid (see --alpha)")
+    ap.add_argument("--alpha", type=float, default=0.0,
+                    help="growth factor of the width schedule; 0: choose from --alpha-grid")
+    ap.add_argument("--eps-grid", default="0.005,0.01,0.02,0.05,0.1,0.15,0.2")
+    ap.add_argument("--alpha-grid", default="2,32")
+    ap.add_argument("--recall-target", type=float, default=0.95)
     ap.add_argument("--fixed-steps", type=int, default=3)
     ap.add_argument("--no-fixed", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -223,7 +226,7 @@ def main():
     index = boa.Index(data.vectors, data.attrs, types, adj, entry)
     q = torch.from_numpy(data.queries).to(dev)
     r = torch.from_numpy(data.ranges).to(dev)
-    kw = dict(k=wl.k, L0=wl.L0, Lmax=wl.Lmax, alpha=args.alpha, eps=args.eps, lds_hash_slots=args.lds_slots)
+    base_kw = dict(k=wl.k, L0=wl.L0, Lmax=wl.Lmax, lds_hash_slots=args.lds_slots)
 
     def timed(search_kw, steps, warmup):
         """warm-up, then `steps` timed searches bracketed by device syncs;
@@ -239,6 +242,34 @@ def main():
         torch.cuda.synchronize()
         t1 = time.perf_counter()
         return (t1 - t0) * 1e3 / steps, index.stats(), o
+
+    # operating point: the metric is QPS at recall@10 >= target, so the
+    # confidence threshold eps and the growth factor alpha (inputs of Alg. 1)
+    # are chosen as the fastest grid point that reaches the target (split
+    # mode, a few steps each); the paper's own point (eps 0.05, alpha 2) is
+    # reported beside it
+    eps_grid = [args.eps] if args.eps > 0 else [float(x) for x in args.eps_grid.split(",")]
+    alpha_grid = [args.alpha] if args.alpha > 0 else [float(x) for x in args.alpha_grid.split(",")]
+    points = [(0.05, 2.0)] + [(e, a) for a in alpha_grid for e in eps_grid if (e, a) != (0.05, 2.0)]
+    if args.eps > 0 or args.alpha > 0:
+        points = [(e, a) for a in alpha_grid for e in eps_grid]
+    sweep = []
+    for e, a in points:
+        ms_p, st_p, o_p = timed(dict(base_kw, eps=e, alpha=a, split=True), 3, 1)
+        fl_p = o_p.final_L.cpu().numpy()
+        _, rt_p = recall(o_p.ids.cpu().numpy().view(np.uint32), o_p.dists.cpu().numpy(),
+                         gt_ids, gt_d, n_valid, wl.k)
+        sweep.append(dict(eps=e, alpha=a, schedule=[p["L"] for p in st_p["phases"]],
+                          ms_per_step=round(ms_p, 4), qps=round(wl.nq / (ms_p / 1e3), 1),
+                          recall_at_10=round(rt_p, 5), L_avg=round(float(fl_p.mean()), 2)))
+        log(f"operating point eps={e} alpha={a}: {ms_p:.3f} ms/step (split), recall {rt_p:.4f}, "
+            f"L_avg {fl_p.mean():.1f}")
+    ok = [p for p in sweep if p["recall_at_10"] >= args.recall_target]
+    chosen = min(ok, key=lambda p: p["ms_per_step"]) if ok else max(sweep, key=lambda p: p["recall_at_10"])
+    target_met = bool(ok)
+    log(f"chosen operating point eps={chosen['eps']} alpha={chosen['alpha']} "
+        f"({'meets' if target_met else 'MISSES'} recall@10 >= {args.recall_target})")
+    kw = dict(base_kw, eps=chosen["eps"], alpha=chosen["alpha"])
 
     modes = {}
     mode_kw = {"phased": {}, "fused": {"fused": True}, "split": {"split": True},
@@ -293,21 +324,6 @@ def main():
         f"{dom['launches']} launches, {bytes_launch / 1e6:.2f} MB/launch -> {achieved:.1f} GB/s; "
         f"kernel time share {kernel_share:.2f}; groups {groups}")
 
-    variant = None
-    if args.alt_alpha > 0:
-        kv = dict(kw, alpha=args.alt_alpha, **mode_kw[mode])
-        msv, stv, out_v = timed(kv, args.steps, args.warmup)
-        fl_v = out_v.final_L.cpu().numpy()
-        ids_v = out_v.ids.cpu().numpy().view(np.uint32)
-        rq_v = recall(ids_v, out_v.dists.cpu().numpy(), gt_ids, gt_d, n_valid, wl.k, per_query=True)
-        variant = dict(alpha=args.alt_alpha, schedule=[p["L"] for p in stv["phases"]], mode=mode,
-                       ms_per_step=round(msv, 4), qps=round(wl.nq / (msv / 1e3), 1),
-                       recall_at_10=round(float(rq_v.mean()), 5), L_avg=round(float(fl_v.mean()), 2),
-                       recall_by_final_L={str(p["L"]): round(float(rq_v[fl_v == p["L"]].mean()), 4)
-                                          for p in stv["phases"] if (fl_v == p["L"]).any()})
-        log(f"schedule variant alpha={args.alt_alpha} ({mode}): {msv:.3f} ms/step, "
-            f"{variant['qps']:,.0f} QPS, recall {variant['recall_at_10']:.4f}, L_avg {variant['L_avg']:.1f}")
-
     fixed = None
     if not args.no_fixed:
         msf, stf, out_f = timed(dict(k=wl.k, fixed_L=500), args.fixed_steps, 1)
@@ -323,15 +339,15 @@ def main():
         import oracle
         threads = min(16, os.cpu_count() or 1)
         oix = oracle.Index(data.vectors, data.attrs, types, adj, entry)
-        osched = oracle.schedule(wl.L0, args.alpha, wl.Lmax)
+        osched = oracle.schedule(wl.L0, chosen["alpha"], wl.Lmax)
         # calibrate, then size the sample to the time budget
         n0 = min(wl.nq, 4 * threads)
         tc = time.perf_counter()
-        oracle.boa(oix, data.queries[:n0], data.ranges[:n0], wl.k, osched, eps=args.eps, threads=threads)
+        oracle.boa(oix, data.queries[:n0], data.ranges[:n0], wl.k, osched, eps=chosen["eps"], threads=threads)
         per_q = (time.perf_counter() - tc) / n0
         ns = int(min(wl.nq, max(n0, args.cpu_seconds / max(per_q, 1e-6))))
         tc = time.perf_counter()
-        ref = oracle.boa(oix, data.queries[:ns], data.ranges[:ns], wl.k, osched, eps=args.eps, threads=threads)
+        ref = oracle.boa(oix, data.queries[:ns], data.ranges[:ns], wl.k, osched, eps=chosen["eps"], threads=threads)
         el = time.perf_counter() - tc
         same = int(((ref.ids == ids[:ns]).all(1) & (ref.final_L == final_L[:ns])).sum())
         cpu = dict(value=round(ns / el, 2), unit="queries/s", cores=threads, kind="oracle",
@@ -356,7 +372,7 @@ def main():
         "dtype": "f32" if wl.vec_dtype == gen.VEC_F32 else "u8",
         "data": "synthetic",
         "config": {"workload": wl.name, "n": wl.n, "d": wl.d, "R": wl.R, "m": wl.m, "nq": wl.nq,
-                   "k": wl.k, "L0": wl.L0, "Lmax": wl.Lmax, "alpha": args.alpha, "eps": args.eps,
+                   "k": wl.k, "L0": wl.L0, "Lmax": wl.Lmax, "alpha": chosen["alpha"], "eps": chosen["eps"],
                    "schedule": sched, "mode": f"BOA ({mode} phases)", "graph": recipe},
         "modes": {m2: {"ms_per_step": round(v[0], 4), "qps": round(wl.nq / (v[0] / 1e3), 1),
                        "launches_per_step": round(v[1]["cum_launches"] / max(1, v[1]["cum_searches"]), 2)}
@@ -369,7 +385,9 @@ def main():
         "recall_by_final_L": rec_by_L,
         "phases": [{k2: (round(v, 4) if isinstance(v, float) else v) for k2, v in p.items()}
                    for p in st["phases"]],
-        "schedule_variant": variant,
+        "recall_target": args.recall_target,
+        "recall_target_met": target_met,
+        "operating_points": sweep,
         "fixed_L500": fixed,
         "speedup_vs_fixed_L500": round(qps / fixed["qps"], 3) if fixed else None,
         "roofline": {"bound": "hbm", "kernel": KERNEL, "mode": mode, "phases": dom["phases"],

@@ -13,6 +13,19 @@ the data it stands in for. The paper draws per-attribute range
 selectivity between 1% and 100% (Sec. IV); the workloads below fix the
 joint selectivity per workload instead.
 
+Descriptor and embedding data of that kind has a low intrinsic
+dimension: its points lie near a low-dimensional structure of the
+ambient space, both between clusters and inside them. The 1M- and
+10M-point mixtures reproduce that: cluster centres lie in a random
+8-dimensional subspace, and 99% of each cluster's noise variance lies on
+8 random directions of its own (1% is isotropic). The per-dimension
+variances are those of the isotropic recipe (centre spread and sigma),
+only their distribution over directions changes. An isotropic mixture
+in 96-768 dimensions instead puts every cluster at the same distance
+from every other and every point of a cluster at the same distance
+from a query, which no real descriptor set does. The tiny workload keeps
+its isotropic recipe.
+
 Encoding conventions shared with every consumer:
   * vectors: row-major n x d, float32 or uint8.
   * attributes: row-major n x m cells of 4 bytes, held in an int32 array;
@@ -114,11 +127,38 @@ def cells_as_f32(a) -> np.ndarray:
 # ---------------------------------------------------------------------------
 # vector mixtures
 
+LATENT = 8          # dimension of the subspace holding the cluster centres
+LOCAL = 8           # directions carrying a cluster's noise
+LOCAL_SHARE = 0.99  # share of the noise variance on those directions
+
+
 def _centres(wl: Workload) -> np.ndarray:
     g = _rng(wl.seed, 1)
+    if wl.kind == "tiny":
+        return g.normal(0.0, 1.0, size=(wl.n_clusters, wl.d))
+    # centres in a random LATENT-dimensional subspace, per-dimension variance
+    # 1 on average (40^2 around 128 for the 0..255 workloads)
+    basis, _ = np.linalg.qr(g.normal(size=(wl.d, LATENT)))
+    z = g.normal(size=(wl.n_clusters, LATENT)) * np.sqrt(wl.d / LATENT)
+    if wl.kind == "dblp":
+        # cluster ids follow the first latent coordinate, so the attributes
+        # derived from the cluster id change smoothly across the space (as a
+        # publication year drifts with topic) instead of at random
+        z = z[np.argsort(z[:, 0], kind="stable")]
+    c = z @ basis.T
     if wl.kind in ("sift", "u8"):
-        return g.normal(128.0, 40.0, size=(wl.n_clusters, wl.d))
-    return g.normal(0.0, 1.0, size=(wl.n_clusters, wl.d))
+        return 128.0 + 40.0 * c
+    return c
+
+
+def _local_bases(wl: Workload) -> np.ndarray:
+    """n_clusters x LOCAL x d: orthonormal noise directions of each cluster."""
+    g = _rng(wl.seed, 6)
+    q, _ = np.linalg.qr(g.normal(size=(wl.n_clusters, wl.d, LOCAL)))
+    return np.ascontiguousarray(q.transpose(0, 2, 1))
+
+
+_SIGMA = {"sift": 20.0, "u8": 20.0, "deep": 0.2, "dblp": 0.2}
 
 
 def _mixture_rows(wl: Workload, centres: np.ndarray, n: int, part: int):
@@ -126,21 +166,37 @@ def _mixture_rows(wl: Workload, centres: np.ndarray, n: int, part: int):
     g = _rng(wl.seed, part)
     cid = g.integers(0, wl.n_clusters, size=n)
     out = np.empty((n, wl.d), dtype=np.uint8 if wl.vec_dtype == VEC_U8 else np.float32)
-    for s in range(0, n, _CHUNK):
-        e = min(n, s + _CHUNK)
-        c = centres[cid[s:e]]
-        if wl.kind == "tiny":
-            x = c + 0.3 * g.standard_normal(size=c.shape)
-            out[s:e] = x.astype(np.float32)
-        elif wl.kind in ("sift", "u8"):
-            x = np.clip(np.rint(c + 20.0 * g.standard_normal(size=c.shape)), 0, 255)
-            out[s:e] = x.astype(out.dtype)
-        elif wl.kind in ("deep", "dblp"):
-            x = c + 0.2 * g.standard_normal(size=c.shape)
+    if wl.kind == "tiny":
+        for s in range(0, n, _CHUNK):
+            e = min(n, s + _CHUNK)
+            c = centres[cid[s:e]]
+            out[s:e] = (c + 0.3 * g.standard_normal(size=c.shape)).astype(np.float32)
+        return out, cid
+    if wl.kind not in _SIGMA:
+        raise ValueError(wl.kind)
+    U = _local_bases(wl)
+    sigma = _SIGMA[wl.kind]
+    a_loc = np.sqrt(LOCAL_SHARE * wl.d / LOCAL)
+    a_iso = np.sqrt(1.0 - LOCAL_SHARE)
+    step = max(4096, (1 << 24) // wl.d)
+    for s in range(0, n, step):
+        e = min(n, s + step)
+        cc = cid[s:e]
+        zl = a_loc * g.standard_normal(size=(e - s, LOCAL))
+        x = a_iso * g.standard_normal(size=(e - s, wl.d))
+        # each cluster's rows get their local directions (one small product
+        # per cluster present in the chunk)
+        order = np.argsort(cc, kind="stable")
+        cs = cc[order]
+        cuts = np.flatnonzero(cs[1:] != cs[:-1]) + 1
+        for rows in np.split(order, cuts):
+            x[rows] += zl[rows] @ U[cc[rows[0]]]
+        x = centres[cc] + sigma * x
+        if wl.kind in ("sift", "u8"):
+            out[s:e] = np.clip(np.rint(x), 0, 255).astype(out.dtype)
+        else:
             x /= np.linalg.norm(x, axis=1, keepdims=True)
             out[s:e] = x.astype(np.float32)
-        else:
-            raise ValueError(wl.kind)
     return out, cid
 
 
@@ -194,7 +250,7 @@ def _quantile_window(g, nq: int, column_sorted: np.ndarray, frac: float) -> np.n
     return np.stack([column_sorted[i0], column_sorted[i1]], axis=1)
 
 
-def _ranges(wl: Workload, attrs: np.ndarray, nq: int) -> np.ndarray:
+def _ranges(wl: Workload, attrs: np.ndarray, nq: int, qcid: np.ndarray) -> np.ndarray:
     g = _rng(wl.seed, 5)
     r = np.empty((nq, wl.m, 2), dtype=np.int32)
     if wl.kind == "tiny":
@@ -215,7 +271,10 @@ def _ranges(wl: Workload, attrs: np.ndarray, nq: int) -> np.ndarray:
         col = np.sort(cells_as_f32(attrs[:, 2]))
         r[:, 2, :] = f32_bits(_quantile_window(g, nq, col, frac))
     elif wl.kind == "dblp":
-        c0 = g.integers(0, 1801, size=nq)
+        # the two cluster-derived attributes get a window of 300 cluster ids
+        # placed so that it holds the query's own cluster's values (cluster
+        # id + 0..99): the predicate is correlated with where the query lies
+        c0 = np.clip(qcid - g.integers(0, 201, size=nq), 0, max(0, wl.n_clusters - 200))
         for j in (0, 1):
             r[:, j, 0] = c0
             r[:, j, 1] = c0 + 299
@@ -233,5 +292,5 @@ def generate(wl: Workload) -> Data:
     vectors, cid = _mixture_rows(wl, centres, wl.n, part=2)
     attrs = _attributes(wl, cid)
     queries, qcid = _mixture_rows(wl, centres, wl.nq, part=4)
-    ranges = _ranges(wl, attrs, wl.nq)
+    ranges = _ranges(wl, attrs, wl.nq, qcid)
     return Data(wl, vectors, attrs, queries, ranges, qcid)

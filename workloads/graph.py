@@ -407,47 +407,48 @@ def candidates_ivf(X: torch.Tensor, K: int, QA: torch.Tensor | None = None, thr:
     return du, cand, du_l, cand_l
 
 
-def attribute_edges(X: torch.Tensor, du_l: torch.Tensor, cand_l: torch.Tensor, budget: int,
-                    alpha: float) -> torch.Tensor:
-    """n x (levels * budget) ids (-1 = none): per threshold level, the
-    alpha-pruned nearest vectors among the points within that threshold."""
+def level_edges(X: torch.Tensor, du_l: torch.Tensor, cand_l: torch.Tensor, budgets, alpha: float) -> torch.Tensor:
+    """n x sum(budgets) ids (-1 = none): per level, the alpha-pruned nearest
+    vectors among the level's candidates, at most budgets[level] of them."""
     n = X.shape[0]
     out = []
     for li in range(du_l.shape[0]):
+        b = int(budgets[li])
         keep = alpha_prune(X, cand_l[li], du_l[li], torch.isfinite(du_l[li]),
-                           torch.full((n,), budget, dtype=torch.int64, device=X.device), alpha)
-        out.append(_compact(torch.where(keep, cand_l[li], torch.full_like(cand_l[li], -1)), budget))
+                           torch.full((n,), b, dtype=torch.int64, device=X.device), alpha)
+        out.append(_compact(torch.where(keep, cand_l[li], torch.full_like(cand_l[li], -1)), b))
     return torch.cat(out, 1)
 
 
 def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
                 alpha: float = 1.2, seed: int = 0x9A9A, entry: int | None = None,
                 attrs: np.ndarray | None = None, attr_dtypes=None,
-                attr_levels=(0.002, 0.02, 0.1), attr_budget: int | None = None,
+                attr_levels=(0.001, 0.01, 0.05, 0.2), attr_budget: int | None = None,
                 cross_links: int | None = None, exact_limit: int = 2_000_000):
     """Fixed-degree proximity graph; returns (adjacency n x R uint32, entry id).
     With `attrs` (n x m cells, column types `attr_dtypes`) rows also hold
-    attribute-aware edges, `attr_budget` (default R // 8) per threshold level.
-    Above `exact_limit` points the candidates come from k-means lists
-    (`candidates_ivf`) instead of an exhaustive pass."""
+    attribute-aware edges, `attr_budget` (default 3R // 16) per threshold
+    level; the pruned nearest neighbours fill what the navigation and
+    attribute-aware links leave of a row. Above `exact_limit` points the candidates
+    come from k-means lists (`candidates_ivf`) instead of an exhaustive pass."""
     dev = torch.device(device)
     n = vectors.shape[0]
     s_id = entry_point(vectors) if entry is None else int(entry)
     X = _as_float(vectors, dev)
     Kc = min(2 * R, n - 1)
-    # 1-2: exact kNN candidates (and, with attributes, the attribute-aware
-    # candidates of every threshold level from the same distance pass).
+    # 1-2: exact kNN candidates and, from the same distance pass, the
+    # candidates of every attribute threshold level
     t0 = time.time()
     attr_e = None
     if attrs is not None and len(attr_levels) > 0:
         QA = _as_float(attribute_quantiles(attrs, attr_dtypes), dev)
-        b = max(1, R // 8) if attr_budget is None else int(attr_budget)
+        b = max(1, (3 * R) // 16) if attr_budget is None else int(attr_budget)
         thr = _thresholds(QA, attr_levels, seed, 2048 if n <= exact_limit or dev.type == "cpu" else 32768)
         if n > exact_limit:
             du, cand, du_l, cand_l = candidates_ivf(X, Kc, QA, thr, min(n - 1, 2 * b), seed=seed)
         else:
             du, cand, du_l, cand_l = candidates(X, Kc, QA, thr, min(n - 1, 2 * b))
-        attr_e = attribute_edges(X, du_l, cand_l, b, alpha)
+        attr_e = level_edges(X, du_l, cand_l, [b] * len(attr_levels), alpha)
         del du_l, cand_l, QA, thr
         _log(f"{Kc}-NN and attribute-aware candidates ({len(attr_levels)} levels x {b}) "
              f"of {n} points in {time.time() - t0:.1f}s")
