@@ -444,9 +444,10 @@ int stage_profile_end(unsigned long long *prof, size_t pn, int L, int waves, hip
     std::fprintf(stderr,
                  "[stage-profile] L=%d waves=%d expansions=%.0f cycles/expansion: select %.0f "
                  "visit %.0f score %.0f sort %.0f rank %.0f rebuild %.0f | spilled %.2f chunks %.2f "
-                 "row-prefetch hit %.2f reissued %.2f\n",
+                 "row-prefetch hit %.2f reissued %.2f | visit: row %.0f table %.0f; no new candidate %.2f\n",
                  L, waves, tot[10], tot[0] / ne, tot[1] / ne, tot[2] / ne, tot[3] / ne, tot[4] / ne,
-                 tot[5] / ne, tot[6] / ne, tot[7] / ne, tot[8] / ne, tot[9] / ne);
+                 tot[5] / ne, tot[6] / ne, tot[7] / ne, tot[8] / ne, tot[9] / ne, tot[12] / ne, tot[13] / ne,
+                 tot[14] / ne);
     (void)hipFree(prof);
     return BOA_OK;
 }

@@ -8,7 +8,7 @@
 
 #define BOA_PAD 0xFFFFFFFFu
 #define BOA_STATUS_OVERFLOW 1u
-#define BOA_PROF_SLOTS 12
+#define BOA_PROF_SLOTS 16
 
 namespace boa {
 

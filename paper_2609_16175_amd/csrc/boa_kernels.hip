@@ -87,6 +87,28 @@ __device__ __forceinline__ uint32_t lower_bound64(const uint64_t *a, uint32_t n,
     }
     return lo;
 }
+// the same index by an eight-way search: seven independent LDS reads per
+// step, so a lone wave waits for a third as many round trips (512 entries:
+// three steps instead of nine)
+__device__ __forceinline__ uint32_t lower_bound64_8way(const uint64_t *a, uint32_t n, uint64_t key)
+{
+    uint32_t lo = 0, hi = n;   // the answer lies in [lo, hi]
+    while (hi - lo > 7u) {
+        const uint32_t q = (hi - lo) >> 3;
+        uint32_t below = 0;    // pivots lo + i q (i = 1..7) holding a key < key
+#pragma unroll
+        for (uint32_t i = 1; i <= 7; ++i) below += a[lo + i * q] < key ? 1u : 0u;
+        // keys are sorted, so the pivots below key are the first `below` ones
+        const uint32_t nlo = below == 0u ? lo : lo + below * q + 1u;
+        hi = below == 7u ? hi : lo + (below + 1u) * q;
+        lo = nlo;
+    }
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (a[mid] < key) lo = mid + 1u; else hi = mid;
+    }
+    return lo;
+}
 // number of entries of a[0, n) that are <= x (a sorted ascending)
 __device__ __forceinline__ uint32_t upper_bound32(const uint32_t *a, uint32_t n, uint32_t x)
 {
@@ -122,6 +144,7 @@ template <int T, int W = 1>
 struct F32Scorer {
     // lane p = lane & 15 accumulates float4 chunks p, p+16, p+32, ...
     static constexpr int kGroup = 16;
+    static constexpr bool kWide = W == 2;
     float4 q[T];
 
     __device__ __forceinline__ void load_query(const void *Q, uint32_t qi, int d, int lane)
@@ -144,23 +167,34 @@ struct F32Scorer {
         const float *vec = reinterpret_cast<const float *>(V);
         const int g = lane >> 4, p = lane & 15, nch = d >> 2;
         for (int r0 = 0; r0 < c; r0 += 4 * RU) {
+            // every candidate id of the round first (independent LDS reads),
+            // then the rows: unconditional loads from valid global addresses
+            // (a lane past the candidates re-reads candidate 0, a chunk past
+            // the row end re-reads its last chunk), masked afterwards
+            uint32_t idv[RU];
+#pragma unroll
+            for (int u = 0; u < RU; ++u) {
+                const int cj = r0 + 4 * u + g;
+                idv[u] = cid[cj < c ? cj : 0];
+            }
             float4 x[RU][T];
 #pragma unroll
             for (int u = 0; u < RU; ++u) {
-                int cj = r0 + 4 * u + g;
-                uint32_t id = cj < c ? cid[cj] : 0u;
-                const float4 *row = reinterpret_cast<const float4 *>(vec + (size_t)id * d);
+                if (r0 + 4 * u < c) {   // uniform: a candidate left in this round
+                    const float4 *row = reinterpret_cast<const float4 *>(vec + (size_t)idv[u] * d);
 #pragma unroll
-                for (int t = 0; t < T; ++t) {
-                    int cc = p + 16 * t;
-                    float4 val = q[t];
-                    if (cj < c && cc < nch) val = row[cc];
-                    x[u][t] = val;
+                    for (int t = 0; t < T; ++t) {
+                        const int cc = p + 16 * t;
+                        x[u][t] = row[cc < nch ? cc : nch - 1];
+                    }
                 }
             }
 #pragma unroll
             for (int u = 0; u < RU; ++u) {
                 if (r0 + 4 * u >= c) break;   // uniform: no candidate left in this round
+#pragma unroll
+                for (int t = 0; t < T; ++t)
+                    if (p + 16 * t >= nch) x[u][t] = q[t];   // past the row end: adds zero
                 float acc = 0.0f;
 #pragma unroll
                 for (int t = 0; t < T; ++t) {
@@ -192,6 +226,7 @@ struct U8Scorer {
     // lane p = lane % G holds the query's 16-byte chunk p (p < d/16); the
     // exact int32 sum is order-free.
     static constexpr int kGroup = G;
+    static constexpr bool kWide = W == 2;
     uint4 q;
 
     __device__ __forceinline__ void load_query(const void *Q, uint32_t qi, int d, int lane)
@@ -219,18 +254,24 @@ struct U8Scorer {
         const uint8_t *vec = reinterpret_cast<const uint8_t *>(V);
         const int g = lane / G, p = lane % G, nch = d >> 4;
         for (int r0 = 0; r0 < c; r0 += PER * RU) {
+            // ids first, then unconditional loads from valid addresses, masked
+            // afterwards (as in F32Scorer)
+            uint32_t idv[RU];
+#pragma unroll
+            for (int u = 0; u < RU; ++u) {
+                const int cj = r0 + PER * u + g;
+                idv[u] = cid[cj < c ? cj : 0];
+            }
             uint4 x[RU];
 #pragma unroll
             for (int u = 0; u < RU; ++u) {
-                int cj = r0 + PER * u + g;
-                uint32_t id = cj < c ? cid[cj] : 0u;
-                uint4 val = q;
-                if (cj < c && p < nch) val = reinterpret_cast<const uint4 *>(vec + (size_t)id * d)[p];
-                x[u] = val;
+                if (r0 + PER * u < c)   // uniform
+                    x[u] = reinterpret_cast<const uint4 *>(vec + (size_t)idv[u] * d)[p < nch ? p : nch - 1];
             }
 #pragma unroll
             for (int u = 0; u < RU; ++u) {
                 if (r0 + PER * u >= c) break;   // uniform: no candidate left in this round
+                if (p >= nch) x[u] = q;         // lanes past the row: add zero
                 int32_t acc = sq4(x[u].x, q.x) + sq4(x[u].y, q.y) + sq4(x[u].z, q.z) + sq4(x[u].w, q.w);
                 // exact integer sum over the group; the group's top lane holds it
 #pragma unroll
@@ -478,15 +519,21 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                     // sort the survivors: each one's rank is the number of
                     // survivors below it (keys are distinct), read back from
                     // LDS as broadcasts, two keys per read
-                    if (key != KEY_NONE) nkey[lanes_below(keep)] = key;
+                    // survivors first, the other lanes' KEY_NONE after them, so
+                    // that reads past the survivors compare false
+                    nkey[key != KEY_NONE ? lanes_below(keep) : kept + lanes_below(~keep)] = key;
                     wave_sync();
                     uint32_t rank = 0;
                     {
+                        // eight keys per step: four independent LDS reads in flight
                         const ulonglong2 *nk2 = reinterpret_cast<const ulonglong2 *>(nkey);
-                        for (uint32_t i = 0; i < kept; i += 2) {
-                            const ulonglong2 pr = nk2[i >> 1];
-                            rank += pr.x < key ? 1u : 0u;
-                            rank += (i + 1 < kept && pr.y < key) ? 1u : 0u;
+                        for (uint32_t i = 0; i < kept; i += 8) {
+                            const ulonglong2 a0 = nk2[(i >> 1) + 0], a1 = nk2[(i >> 1) + 1];
+                            const ulonglong2 a2 = nk2[(i >> 1) + 2], a3 = nk2[(i >> 1) + 3];
+                            rank += (a0.x < key ? 1u : 0u) + (a0.y < key ? 1u : 0u);
+                            rank += (a1.x < key ? 1u : 0u) + (a1.y < key ? 1u : 0u);
+                            rank += (a2.x < key ? 1u : 0u) + (a2.y < key ? 1u : 0u);
+                            rank += (a3.x < key ? 1u : 0u) + (a3.y < key ? 1u : 0u);
                         }
                     }
                     wave_sync();
@@ -510,7 +557,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                     uint32_t f = 0xFFFFFFFFu;
                     uint32_t pos = 0;
                     if (lane < (int)kept) {
-                        pos = lower_bound64(beam, len, key);
+                        pos = Scorer::kWide ? lower_bound64_8way(beam, len, key) : lower_bound64(beam, len, key);
                         f = pos + lane;
                     }
                     const uint32_t p0 = bcast0(pos);
@@ -576,7 +623,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             const uint32_t u = key_id(ku);
             E += 1;
 
-            // ---- adjacency row (prefetched if predicted), then the next prediction
+            // ---- adjacency row (prefetched if predicted)
             uint32_t v;
             if (u == pf_id) {
                 v = pf_row;
@@ -584,13 +631,12 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             } else {
                 v = lane < R ? ix.adj[(size_t)u * R + lane] : BOA_PAD;
             }
-            pf_key = kn;
-            pf_id = BOA_PAD;
-            if (j2 >= 0) {
-                pf_id = key_id(kn);
-                pf_row = lane < R ? ix.adj[(size_t)pf_id * R + lane] : BOA_PAD;
-            }
             PROF_ADD(10, 1);
+#ifdef BOA_STAGE_PROFILE
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // row in hand, for the split below
+#endif
+            PROF_T(t_row);
+            PROF_ADD(12, t_row - t_sel1);
 
             // ---- test-and-insert into the visited set
             int vst = 0;
@@ -602,10 +648,22 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                 }
                 if (vst < 0) vst = visit_bits(vs, v) ? 1 : 0;
             }
+            PROF_T(t_vl);
+            PROF_ADD(13, t_vl - t_row);
             const bool is_new = vst > 0;
             const uint64_t nm = __ballot(is_new);
             c = __popcll(nm);
+            PROF_ADD(14, c == 0 ? 1 : 0);
             if (is_new) cid[lanes_below(nm)] = v;
+            // the row of the entry expected next is requested only now: a
+            // load issued before the visited test would be waited for there
+            // (loads retire in order), while from here it overlaps the gathers
+            pf_key = kn;
+            pf_id = BOA_PAD;
+            if (j2 >= 0) {
+                pf_id = key_id(kn);
+                pf_row = lane < R ? ix.adj[(size_t)pf_id * R + lane] : BOA_PAD;
+            }
             PROF_T(t_vis1);
             PROF_ADD(1, t_vis1 - t_sel1);
             PROF_ADD(6, spill ? 1 : 0);

@@ -140,11 +140,6 @@ def _centres(wl: Workload) -> np.ndarray:
     # 1 on average (40^2 around 128 for the 0..255 workloads)
     basis, _ = np.linalg.qr(g.normal(size=(wl.d, LATENT)))
     z = g.normal(size=(wl.n_clusters, LATENT)) * np.sqrt(wl.d / LATENT)
-    if wl.kind == "dblp":
-        # cluster ids follow the first latent coordinate, so the attributes
-        # derived from the cluster id change smoothly across the space (as a
-        # publication year drifts with topic) instead of at random
-        z = z[np.argsort(z[:, 0], kind="stable")]
     c = z @ basis.T
     if wl.kind in ("sift", "u8"):
         return 128.0 + 40.0 * c

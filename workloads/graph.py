@@ -15,7 +15,11 @@ and it is deliberately not the paper's builder:
      by the same alpha-pruning (so roughly one per nearby component), and
      every point links to its nearest sample points. Clustered mixtures
      otherwise give one disconnected kNN component per cluster;
-  4. connectivity repair: every point is made reachable from the entry
+  4. random-subset levels: for a few fractions f, a seeded subset holding
+     about f of the points, and every point's alpha-pruned nearest members
+     of it. Their spacing grows as f shrinks, so these edges span the data
+     at several scales whatever the attributes are;
+  5. connectivity repair: every point is made reachable from the entry
      point (the point nearest the data centroid).
 
 With attributes given, rows also carry attribute-aware edges in the manner
@@ -255,18 +259,21 @@ def _thresholds(QA: torch.Tensor, levels, seed: int, chunk: int) -> torch.Tensor
 
 
 def candidates(X: torch.Tensor, K: int, QA: torch.Tensor | None = None, thr: torch.Tensor | None = None,
-               K_attr: int = 0, chunk: int = 2048):
-    """One exhaustive pass: every point's K nearest others (dist, ids) and,
-    with attribute quantiles QA and thresholds thr (n x levels), its K_attr
-    nearest among the points within each threshold (levels x n x K_attr,
-    missing = inf / unspecified id). Sorted by (distance, id)."""
+               K_attr: int = 0, chunk: int = 2048, member: torch.Tensor | None = None):
+    """One exhaustive pass: every point's K nearest others (dist, ids) and its
+    K_attr nearest within each level (levels x n x K_attr, missing = inf /
+    unspecified id). The levels are, first, the attribute threshold levels
+    (attribute quantiles QA, thresholds thr: n x levels; a target is in a
+    level when its attribute distance is within the threshold), then the
+    random-subset levels (member: levels x n bool). Sorted by (distance, id)."""
     n = X.shape[0]
     dev = X.device
     nx = (X * X).sum(1)
     kk = min(n, K + 5)
     du = torch.empty((n, K), dtype=X.dtype, device=dev)
     cand = torch.empty((n, K), dtype=torch.int64, device=dev)
-    nl = 0 if thr is None else thr.shape[1]
+    nl_a = 0 if thr is None else thr.shape[1]
+    nl = nl_a + (0 if member is None else member.shape[0])
     ka = min(n, K_attr + 5)
     du_l = torch.empty((nl, n, K_attr), dtype=X.dtype, device=dev)
     cand_l = torch.empty((nl, n, K_attr), dtype=torch.int64, device=dev)
@@ -279,9 +286,10 @@ def candidates(X: torch.Tensor, K: int, QA: torch.Tensor | None = None, thr: tor
         dv, di = _sort_by_dist_then_id(dv, di)
         du[s:e], cand[s:e] = dv[:, :K], di[:, :K]
         if nl:
-            A = _attr_dist(QA[s:e], QA)
+            A = _attr_dist(QA[s:e], QA) if nl_a else None
             for li in range(nl):
-                Dl = torch.where(A > thr[s:e, li:li + 1], torch.full_like(D, float("inf")), D)
+                out = A > thr[s:e, li:li + 1] if li < nl_a else ~member[li - nl_a][None, :]
+                Dl = torch.where(out, torch.full_like(D, float("inf")), D)
                 dv, di = torch.topk(Dl, ka, dim=1, largest=False, sorted=True)
                 dv, di = _sort_by_dist_then_id(dv, di)
                 du_l[li, s:e], cand_l[li, s:e] = dv[:, :K_attr], di[:, :K_attr]
@@ -322,7 +330,8 @@ def kmeans(X: torch.Tensor, C: int, iters: int = 6, sample: int = 1 << 20, seed:
 
 
 def candidates_ivf(X: torch.Tensor, K: int, QA: torch.Tensor | None = None, thr: torch.Tensor | None = None,
-                   K_attr: int = 0, lists: int = 0, nprobe: int = 16, seed: int = 0, batch_elems: int = 1 << 28):
+                   K_attr: int = 0, lists: int = 0, nprobe: int = 16, seed: int = 0, batch_elems: int = 1 << 28,
+                   member: torch.Tensor | None = None):
     """The outputs of `candidates`, searched per k-means list instead of
     exhaustively: the members of each list against the points of its
     `nprobe` nearest lists (itself included). Exact within that pool."""
@@ -341,7 +350,8 @@ def candidates_ivf(X: torch.Tensor, K: int, QA: torch.Tensor | None = None, thr:
     nx = (X * X).sum(1)
     du = torch.full((n, K), float("inf"), dtype=X.dtype, device=dev)
     cand = torch.full((n, K), -1, dtype=torch.int64, device=dev)
-    nl = 0 if thr is None else thr.shape[1]
+    nl_a = 0 if thr is None else thr.shape[1]
+    nl = nl_a + (0 if member is None else member.shape[0])
     du_l = torch.full((nl, n, K_attr), float("inf"), dtype=X.dtype, device=dev)
     cand_l = torch.full((nl, n, K_attr), -1, dtype=torch.int64, device=dev)
     cnt_h = cnt.cpu().numpy()
@@ -393,12 +403,17 @@ def candidates_ivf(X: torch.Tensor, K: int, QA: torch.Tensor | None = None, thr:
         take(D, K, du, cand)
         if nl:
             A = None
-            for j in range(QA.shape[1]):
-                gj = (QA[mid.clamp_min(0), j][:, :, None] - QA[pid.clamp_min(0), j][:, None, :]).abs()
-                A = gj if A is None else torch.maximum(A, gj)
-            th = thr[mid.clamp_min(0)]                      # B x mm x levels
+            if nl_a:
+                for j in range(QA.shape[1]):
+                    gj = (QA[mid.clamp_min(0), j][:, :, None] - QA[pid.clamp_min(0), j][:, None, :]).abs()
+                    A = gj if A is None else torch.maximum(A, gj)
+                th = thr[mid.clamp_min(0)]                      # B x mm x levels
             for li in range(nl):
-                Dl = torch.where(A > th[:, :, li:li + 1], torch.full_like(D, float("inf")), D)
+                if li < nl_a:
+                    out = A > th[:, :, li:li + 1]
+                else:
+                    out = ~member[li - nl_a][pid.clamp_min(0)][:, None, :]
+                Dl = torch.where(out, torch.full_like(D, float("inf")), D)
                 take(Dl, K_attr, du_l[li], cand_l[li])
                 del Dl
             del A
@@ -424,38 +439,52 @@ def build_graph(vectors: np.ndarray, R: int, device: str | torch.device = "cpu",
                 alpha: float = 1.2, seed: int = 0x9A9A, entry: int | None = None,
                 attrs: np.ndarray | None = None, attr_dtypes=None,
                 attr_levels=(0.001, 0.01, 0.05, 0.2), attr_budget: int | None = None,
+                sub_levels=(0.001, 0.01, 0.05), sub_budget: int | None = None,
                 cross_links: int | None = None, exact_limit: int = 2_000_000):
     """Fixed-degree proximity graph; returns (adjacency n x R uint32, entry id).
-    With `attrs` (n x m cells, column types `attr_dtypes`) rows also hold
-    attribute-aware edges, `attr_budget` (default 3R // 16) per threshold
-    level; the pruned nearest neighbours fill what the navigation and
-    attribute-aware links leave of a row. Above `exact_limit` points the candidates
-    come from k-means lists (`candidates_ivf`) instead of an exhaustive pass."""
+    Rows hold, besides the pruned nearest neighbours and the navigation
+    links, `sub_budget` (default R // 32) edges per random-subset level (the
+    alpha-pruned nearest members of a seeded subset holding that fraction of
+    the points: edges at the scale of the subset's spacing) and, with
+    `attrs` (n x m cells, column types `attr_dtypes`), `attr_budget`
+    (default R // 6) attribute-aware edges per threshold level. The pruned
+    nearest neighbours fill what the other links leave of a row. Above
+    `exact_limit` points the candidates come from k-means lists
+    (`candidates_ivf`) instead of an exhaustive pass."""
     dev = torch.device(device)
     n = vectors.shape[0]
     s_id = entry_point(vectors) if entry is None else int(entry)
     X = _as_float(vectors, dev)
     Kc = min(2 * R, n - 1)
     # 1-2: exact kNN candidates and, from the same distance pass, the
-    # candidates of every attribute threshold level
+    # candidates of every random-subset level and attribute threshold level
     t0 = time.time()
-    attr_e = None
+    QA = thr = member = None
+    budgets = []
     if attrs is not None and len(attr_levels) > 0:
         QA = _as_float(attribute_quantiles(attrs, attr_dtypes), dev)
-        b = max(1, (3 * R) // 16) if attr_budget is None else int(attr_budget)
         thr = _thresholds(QA, attr_levels, seed, 2048 if n <= exact_limit or dev.type == "cpu" else 32768)
-        if n > exact_limit:
-            du, cand, du_l, cand_l = candidates_ivf(X, Kc, QA, thr, min(n - 1, 2 * b), seed=seed)
-        else:
-            du, cand, du_l, cand_l = candidates(X, Kc, QA, thr, min(n - 1, 2 * b))
-        attr_e = level_edges(X, du_l, cand_l, [b] * len(attr_levels), alpha)
-        del du_l, cand_l, QA, thr
-        _log(f"{Kc}-NN and attribute-aware candidates ({len(attr_levels)} levels x {b}) "
-             f"of {n} points in {time.time() - t0:.1f}s")
+        budgets += [max(1, R // 6) if attr_budget is None else int(attr_budget)] * len(attr_levels)
+    n_attr_levels = len(budgets)
+    if len(sub_levels) > 0:
+        g = np.random.Generator(np.random.PCG64(seed ^ 0x3C3C))
+        u = g.random((len(sub_levels), n))
+        member = torch.from_numpy(u < np.asarray(sub_levels, dtype=np.float64)[:, None]).to(dev)
+        budgets += [max(1, R // 32) if sub_budget is None else int(sub_budget)] * len(sub_levels)
+    K_l = min(n - 1, 2 * max(budgets)) if budgets else 0
+    if n > exact_limit:
+        du, cand, du_l, cand_l = candidates_ivf(X, Kc, QA, thr, K_l, seed=seed, member=member)
     else:
-        du, cand, _, _ = candidates_ivf(X, Kc, seed=seed) if n > exact_limit else candidates(X, Kc)
-        _log(f"{Kc}-NN candidates of {n} points in {time.time() - t0:.1f}s")
-    R_cross = max(2, R // 4) if cross_links is None else int(cross_links)
+        du, cand, du_l, cand_l = candidates(X, Kc, QA, thr, K_l, member=member)
+    attr_e = None
+    if budgets:
+        # subset edges first in the row, then the attribute-aware ones
+        lev = level_edges(X, du_l, cand_l, budgets, alpha)
+        na = sum(budgets[:n_attr_levels])
+        attr_e = torch.cat([lev[:, na:], lev[:, :na]], 1)
+    del du_l, cand_l, QA, thr, member
+    _log(f"{Kc}-NN candidates and level edges (budgets {budgets}) of {n} points in {time.time() - t0:.1f}s")
+    R_cross = max(2, R // 8) if cross_links is None else int(cross_links)
     R_long = R_cross + 1
     K_nav = max(2, R // 2)
 
