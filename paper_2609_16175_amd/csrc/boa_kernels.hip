@@ -70,6 +70,14 @@ __device__ __forceinline__ void wave_sync()
 
 __device__ __forceinline__ uint32_t bcast0(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// value of lane l (wave-uniform l) in every lane, without an LDS round trip
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 __device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
 {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
@@ -158,25 +166,39 @@ struct F32Scorer {
         }
     }
 
-    __device__ __forceinline__ void score(const void *V, int d, const uint32_t *cid, int c, float *cd, int lane)
+    // rows in flight per round trip: the narrow variant keeps registers for
+    // occupancy; the wide one covers most expansions in one round trip
+    static constexpr int RU = W == 1 ? (T <= 2 ? 4 : (T <= 4 ? 2 : 1))
+                                     : (T <= 2 ? 16 : (T <= 4 ? 8 : (T <= 6 ? 4 : (T <= 12 ? 2 : 1))));
+    struct Ids {
+        uint32_t v[RU];
+    };
+
+    // candidate ids of the round starting at r0 (independent LDS reads; a
+    // lane past the candidates takes candidate 0)
+    __device__ __forceinline__ void read_ids(const uint32_t *cid, int c, int r0, int lane, Ids &ids) const
     {
-        // rows in flight per round trip: the narrow variant keeps registers
-        // for occupancy; the wide one covers most expansions in one round trip
-        constexpr int RU = W == 1 ? (T <= 2 ? 4 : (T <= 4 ? 2 : 1))
-                                  : (T <= 2 ? 16 : (T <= 4 ? 8 : (T <= 6 ? 4 : (T <= 12 ? 2 : 1))));
+        const int g = lane >> 4;
+#pragma unroll
+        for (int u = 0; u < RU; ++u) {
+            const int cj = r0 + 4 * u + g;
+            ids.v[u] = cid[cj < c ? cj : 0];
+        }
+    }
+
+    // `first` holds the ids of the first round, read by the caller together
+    // with its own reads of the candidate list
+    __device__ __forceinline__ void score(const void *V, int d, const uint32_t *cid, int c, float *cd, int lane,
+                                          const Ids &first)
+    {
         const float *vec = reinterpret_cast<const float *>(V);
         const int g = lane >> 4, p = lane & 15, nch = d >> 2;
         for (int r0 = 0; r0 < c; r0 += 4 * RU) {
-            // every candidate id of the round first (independent LDS reads),
-            // then the rows: unconditional loads from valid global addresses
-            // (a lane past the candidates re-reads candidate 0, a chunk past
-            // the row end re-reads its last chunk), masked afterwards
-            uint32_t idv[RU];
-#pragma unroll
-            for (int u = 0; u < RU; ++u) {
-                const int cj = r0 + 4 * u + g;
-                idv[u] = cid[cj < c ? cj : 0];
-            }
+            // the rows: unconditional loads from valid global addresses (a
+            // chunk past the row end re-reads its last chunk), masked afterwards
+            Ids ids = first;
+            if (r0 > 0) read_ids(cid, c, r0, lane, ids);
+            const uint32_t *idv = ids.v;
             float4 x[RU][T];
 #pragma unroll
             for (int u = 0; u < RU; ++u) {
@@ -192,32 +214,40 @@ struct F32Scorer {
 #pragma unroll
             for (int u = 0; u < RU; ++u) {
                 if (r0 + 4 * u >= c) break;   // uniform: no candidate left in this round
-#pragma unroll
-                for (int t = 0; t < T; ++t)
-                    if (p + 16 * t >= nch) x[u][t] = q[t];   // past the row end: adds zero
-                float acc = 0.0f;
-#pragma unroll
-                for (int t = 0; t < T; ++t) {
-                    float a0 = x[u][t].x - q[t].x;
-                    acc = __builtin_fmaf(a0, a0, acc);
-                    float a1 = x[u][t].y - q[t].y;
-                    acc = __builtin_fmaf(a1, a1, acc);
-                    float a2 = x[u][t].z - q[t].z;
-                    acc = __builtin_fmaf(a2, a2, acc);
-                    float a3 = x[u][t].w - q[t].w;
-                    acc = __builtin_fmaf(a3, a3, acc);
-                }
-                // pairwise tree over the 16 partials (p += p+8, +4, +2, +1),
-                // mirrored onto the row's top lanes: lane 15 ends with the
-                // same sums in the same order (each add is commutative)
-                acc = acc + from_lane_minus_f<8>(acc);
-                acc = acc + from_lane_minus_f<4>(acc);
-                acc = acc + from_lane_minus_f<2>(acc);
-                acc = acc + from_lane_minus_f<1>(acc);
-                int cj = r0 + 4 * u + g;
+                const float acc = dist(x[u], p, nch);
+                const int cj = r0 + 4 * u + g;
                 if (p == 15 && cj < c) cd[cj] = acc;
             }
         }
+    }
+
+    // squared distance of one row held by a 16-lane group (chunk p + 16 t in
+    // x[t]); lane 15 of the group returns it
+    __device__ __forceinline__ float dist(float4 (&x)[T], int p, int nch) const
+    {
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+            if (p + 16 * t >= nch) x[t] = q[t];   // past the row end: adds zero
+        float acc = 0.0f;
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            float a0 = x[t].x - q[t].x;
+            acc = __builtin_fmaf(a0, a0, acc);
+            float a1 = x[t].y - q[t].y;
+            acc = __builtin_fmaf(a1, a1, acc);
+            float a2 = x[t].z - q[t].z;
+            acc = __builtin_fmaf(a2, a2, acc);
+            float a3 = x[t].w - q[t].w;
+            acc = __builtin_fmaf(a3, a3, acc);
+        }
+        // pairwise tree over the 16 partials (p += p+8, +4, +2, +1), mirrored
+        // onto the row's top lanes: lane 15 ends with the same sums in the
+        // same order (each add is commutative)
+        acc = acc + from_lane_minus_f<8>(acc);
+        acc = acc + from_lane_minus_f<4>(acc);
+        acc = acc + from_lane_minus_f<2>(acc);
+        acc = acc + from_lane_minus_f<1>(acc);
+        return acc;
     }
 };
 
@@ -247,21 +277,33 @@ struct U8Scorer {
         return s;
     }
 
-    __device__ __forceinline__ void score(const void *V, int d, const uint32_t *cid, int c, float *cd, int lane)
+    static constexpr int PER = 64 / G;   // candidates per round
+    static constexpr int RU = W == 1 ? (G <= 8 ? 2 : 4) : (G <= 16 ? G : 16);
+    struct Ids {
+        uint32_t v[RU];
+    };
+
+    __device__ __forceinline__ void read_ids(const uint32_t *cid, int c, int r0, int lane, Ids &ids) const
     {
-        constexpr int PER = 64 / G;            // candidates per round
-        constexpr int RU = W == 1 ? (G <= 8 ? 2 : 4) : (G <= 16 ? G : 16);
+        const int g = lane / G;
+#pragma unroll
+        for (int u = 0; u < RU; ++u) {
+            const int cj = r0 + PER * u + g;
+            ids.v[u] = cid[cj < c ? cj : 0];
+        }
+    }
+
+    __device__ __forceinline__ void score(const void *V, int d, const uint32_t *cid, int c, float *cd, int lane,
+                                          const Ids &first)
+    {
         const uint8_t *vec = reinterpret_cast<const uint8_t *>(V);
         const int g = lane / G, p = lane % G, nch = d >> 4;
         for (int r0 = 0; r0 < c; r0 += PER * RU) {
-            // ids first, then unconditional loads from valid addresses, masked
-            // afterwards (as in F32Scorer)
-            uint32_t idv[RU];
-#pragma unroll
-            for (int u = 0; u < RU; ++u) {
-                const int cj = r0 + PER * u + g;
-                idv[u] = cid[cj < c ? cj : 0];
-            }
+            // unconditional loads from valid addresses, masked afterwards (as
+            // in F32Scorer)
+            Ids ids = first;
+            if (r0 > 0) read_ids(cid, c, r0, lane, ids);
+            const uint32_t *idv = ids.v;
             uint4 x[RU];
 #pragma unroll
             for (int u = 0; u < RU; ++u) {
@@ -271,19 +313,27 @@ struct U8Scorer {
 #pragma unroll
             for (int u = 0; u < RU; ++u) {
                 if (r0 + PER * u >= c) break;   // uniform: no candidate left in this round
-                if (p >= nch) x[u] = q;         // lanes past the row: add zero
-                int32_t acc = sq4(x[u].x, q.x) + sq4(x[u].y, q.y) + sq4(x[u].z, q.z) + sq4(x[u].w, q.w);
-                // exact integer sum over the group; the group's top lane holds it
-#pragma unroll
-                for (int s = G >> 1; s >= 16; s >>= 1) acc += __shfl_xor(acc, s);
-                if (G >= 16) acc += (int32_t)from_lane_minus<8>((uint32_t)acc);
-                if (G >= 8) acc += (int32_t)from_lane_minus<4>((uint32_t)acc);
-                if (G >= 4) acc += (int32_t)from_lane_minus<2>((uint32_t)acc);
-                if (G >= 2) acc += (int32_t)from_lane_minus<1>((uint32_t)acc);
-                int cj = r0 + PER * u + g;
+                const int32_t acc = dist(x[u], p, nch);
+                const int cj = r0 + PER * u + g;
                 if (p == G - 1 && cj < c) cd[cj] = (float)acc;
             }
         }
+    }
+
+    // exact squared distance of one row held by a G-lane group (16-byte
+    // chunk p in x); the group's top lane returns it
+    __device__ __forceinline__ int32_t dist(uint4 x, int p, int nch) const
+    {
+        if (p >= nch) x = q;   // lanes past the row: add zero
+        int32_t acc = sq4(x.x, q.x) + sq4(x.y, q.y) + sq4(x.z, q.z) + sq4(x.w, q.w);
+        // exact integer sum over the group; the group's top lane holds it
+#pragma unroll
+        for (int s = G >> 1; s >= 16; s >>= 1) acc += __shfl_xor(acc, s);
+        if (G >= 16) acc += (int32_t)from_lane_minus<8>((uint32_t)acc);
+        if (G >= 8) acc += (int32_t)from_lane_minus<4>((uint32_t)acc);
+        if (G >= 4) acc += (int32_t)from_lane_minus<2>((uint32_t)acc);
+        if (G >= 2) acc += (int32_t)from_lane_minus<1>((uint32_t)acc);
+        return acc;
     }
 };
 
@@ -319,16 +369,25 @@ __device__ __forceinline__ uint32_t mix_id(uint32_t v, uint32_t B)
     return (h * 0x85EBCA6Bu) & mask;
 }
 
+// Bit 15 of each 16-bit half of the result is set when that half of w is
+// zero (the masked add sets bit 15 of a half exactly when its low 15 bits
+// are not all zero, and no carry crosses into the other half).
+__device__ __forceinline__ uint32_t zero_halves(uint32_t w)
+{
+    const uint32_t t = (w & 0x7FFF7FFFu) + 0x7FFF7FFFu;
+    return ~(t | w) & 0x80008000u;
+}
+
 __device__ __forceinline__ bool has16(const uint4 &b, uint32_t e)
 {
-    return ((b.x & 0xFFFFu) == e) | ((b.x >> 16) == e) | ((b.y & 0xFFFFu) == e) | ((b.y >> 16) == e) |
-           ((b.z & 0xFFFFu) == e) | ((b.z >> 16) == e) | ((b.w & 0xFFFFu) == e) | ((b.w >> 16) == e);
+    const uint32_t ee = e * 0x00010001u;
+    return (zero_halves(b.x ^ ee) | zero_halves(b.y ^ ee) | zero_halves(b.z ^ ee) | zero_halves(b.w ^ ee)) != 0u;
 }
 
 __device__ __forceinline__ uint32_t empties16(const uint4 &b)
 {
-    return ((b.x & 0xFFFFu) == 0u) + ((b.x >> 16) == 0u) + ((b.y & 0xFFFFu) == 0u) + ((b.y >> 16) == 0u) +
-           ((b.z & 0xFFFFu) == 0u) + ((b.z >> 16) == 0u) + ((b.w & 0xFFFFu) == 0u) + ((b.w >> 16) == 0u);
+    return (uint32_t)__popc(zero_halves(b.x) | (zero_halves(b.y) >> 1) | (zero_halves(b.z) >> 2) |
+                            (zero_halves(b.w) >> 3));
 }
 
 // 1: v was not in the set and now is (in LDS); 0: v was already there;
@@ -342,20 +401,27 @@ __device__ __forceinline__ int visit_lds(const Visited &s, uint32_t v)
     const uint32_t e1 = 0x8000u | r, e2 = 0xC000u | r;
     const uint4 *bk = reinterpret_cast<const uint4 *>(s.words);
     for (int attempt = 0; attempt < 256; ++attempt) {
+        // both buckets read before either is tested: one LDS round trip
         const uint4 B1 = bk[b1], B2 = bk[b2];
-        if (has16(B1, e1) || has16(B2, e2)) return 0;
+        if (has16(B1, e1) | has16(B2, e2)) return 0;
         const uint32_t n1 = empties16(B1), n2 = empties16(B2);
         if (n1 == 0u && n2 == 0u) return -1;
         const bool use1 = n1 >= n2;
         const uint4 Bc = use1 ? B1 : B2;
         const uint32_t e = use1 ? e1 : e2;
         const uint32_t bi = use1 ? b1 : b2;
+        // first (lowest) free half-word: the lowest word with a free half,
+        // its low half when that one is free
         const uint32_t w[4] = {Bc.x, Bc.y, Bc.z, Bc.w};
         uint32_t wi = 0, old = 0, neu = 0;
 #pragma unroll
-        for (int q = 3; q >= 0; --q) {   // first (lowest) free half-word
-            if ((w[q] >> 16) == 0u) { wi = q; old = w[q]; neu = w[q] | (e << 16); }
-            if ((w[q] & 0xFFFFu) == 0u) { wi = q; old = w[q]; neu = w[q] | e; }
+        for (int q = 3; q >= 0; --q) {
+            const uint32_t zq = zero_halves(w[q]);
+            if (zq) {
+                wi = q;
+                old = w[q];
+                neu = w[q] | ((zq & 0x8000u) ? e : (e << 16));
+            }
         }
         if (atomicCAS(&s.words[bi * 4u + wi], old, neu) == old) return 1;
         // another lane changed that word: look again
@@ -421,6 +487,39 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     const uint32_t table_words = (1u << a.h_log2) >> 1;
 
     Scorer sc;
+    // one point's attribute record (m_pad cells) and its violation count
+    auto load_attrs = [&](uint32_t id, int4 &w0, int4 &w1) {
+        const int32_t *ar = ix.attrs + (size_t)id * ix.m_pad;
+        if (ix.m_pad >= 4) {
+            w0 = reinterpret_cast<const int4 *>(ar)[0];
+            if (ix.m_pad == 8) w1 = reinterpret_cast<const int4 *>(ar)[1];
+        } else if (ix.m_pad == 2) {
+            const int2 t2 = reinterpret_cast<const int2 *>(ar)[0];
+            w0.x = t2.x;
+            w0.y = t2.y;
+        } else {
+            w0.x = ar[0];
+        }
+    };
+    int32_t lo[BOA_MAX_M], hi[BOA_MAX_M];
+    auto count_phi = [&](const int4 &w0, const int4 &w1) -> uint32_t {
+        const int32_t av[BOA_MAX_M] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+        uint32_t phi = 0;
+#pragma unroll
+        for (int j = 0; j < BOA_MAX_M; ++j) {
+            if (j < m) {
+                bool ok;
+                if ((ix.f32_mask >> j) & 1u) {
+                    const float x = __int_as_float(av[j]);
+                    ok = (__int_as_float(lo[j]) <= x) && (x <= __int_as_float(hi[j]));
+                } else {
+                    ok = (lo[j] <= av[j]) && (av[j] <= hi[j]);
+                }
+                phi += ok ? 0u : 1u;
+            }
+        }
+        return phi;
+    };
 #ifdef BOA_STAGE_PROFILE
     uint64_t prof_acc[BOA_PROF_SLOTS] = {};
 #endif
@@ -432,7 +531,6 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         const uint32_t qi = bcast0(a.active[t]);
 
         sc.load_query(a.queries, qi, d, lane);
-        int32_t lo[BOA_MAX_M], hi[BOA_MAX_M];
 #pragma unroll
         for (int j = 0; j < BOA_MAX_M; ++j) {
             lo[j] = j < m ? a.ranges[((size_t)qi * m + j) * 2 + 0] : 0;
@@ -450,6 +548,19 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         wave_sync();
 
         bool spill = false;
+        // test-and-insert of this lane's neighbour: 1 new, 0 seen (or padding)
+        auto visit_test = [&](uint32_t v) -> int {
+            int vst = 0;
+            if (v != BOA_PAD) vst = visit_lds(vs, v);
+            if (__ballot(vst < 0) != 0ull) {
+                if (!spill) {          // first overflow of this query: reset the bitmap
+                    spill = true;
+                    clear_bits(vs, lane);
+                }
+                if (vst < 0) vst = visit_bits(vs, v) ? 1 : 0;
+            }
+            return vst;
+        };
         uint32_t E = 0, S = 0;
         uint32_t len = 0;
         int expanded_j = -1;
@@ -472,46 +583,24 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             if (c > 0) {
                 wave_sync();
                 S += c;
-                // attribute records first, then the vectors, so that both
-                // gathers are in flight together; phi is counted afterwards
-                int4 w0 = make_int4(0, 0, 0, 0), w1 = make_int4(0, 0, 0, 0);
-                if (lane < (int)c) {
-                    const int32_t *ar = ix.attrs + (size_t)cid[lane] * ix.m_pad;
-                    if (ix.m_pad >= 4) {
-                        w0 = reinterpret_cast<const int4 *>(ar)[0];
-                        if (ix.m_pad == 8) w1 = reinterpret_cast<const int4 *>(ar)[1];
-                    } else if (ix.m_pad == 2) {
-                        int2 t2 = reinterpret_cast<const int2 *>(ar)[0];
-                        w0.x = t2.x;
-                        w0.y = t2.y;
-                    } else {
-                        w0.x = ar[0];
-                    }
-                }
-                sc.score(a.ix.vectors, d, cid, (int)c, cd, lane);
-                uint32_t phi = 0;
+                uint64_t key = KEY_NONE;
                 {
-                    const int32_t av[BOA_MAX_M] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-#pragma unroll
-                    for (int j = 0; j < BOA_MAX_M; ++j) {
-                        if (j < m) {
-                            bool ok;
-                            if ((ix.f32_mask >> j) & 1u) {
-                                float x = __int_as_float(av[j]);
-                                ok = (__int_as_float(lo[j]) <= x) && (x <= __int_as_float(hi[j]));
-                            } else {
-                                ok = (lo[j] <= av[j]) && (av[j] <= hi[j]);
-                            }
-                            phi += ok ? 0u : 1u;
-                        }
-                    }
+                    // attribute records first, then the vectors, so that both
+                    // gathers are in flight together; phi is counted afterwards.
+                    // This lane's candidate (for its attribute record) and the
+                    // scorer's first round of ids: LDS reads issued together
+                    const uint32_t my_id = cid[lane];
+                    typename Scorer::Ids ids0;
+                    sc.read_ids(cid, (int)c, 0, lane, ids0);
+                    int4 w0 = make_int4(0, 0, 0, 0), w1 = make_int4(0, 0, 0, 0);
+                    if (lane < (int)c) load_attrs(my_id, w0, w1);
+                    sc.score(a.ix.vectors, d, cid, (int)c, cd, lane, ids0);
+                    const uint32_t phi = count_phi(w0, w1);
+                    wave_sync();
+                    if (lane < (int)c) key = make_key(phi, cd[lane], cid[lane]);
                 }
-                wave_sync();
                 PROF_T(t_score1);
                 PROF_ADD(2, t_score1 - t_score0);
-
-                uint64_t key = KEY_NONE;
-                if (lane < (int)c) key = make_key(phi, cd[lane], cid[lane]);
                 if (len == (uint32_t)L && key >= beam[L - 1]) key = KEY_NONE;  // cannot enter
                 const uint64_t keep = __ballot(key != KEY_NONE);
                 const uint32_t kept = __popcll(keep);
@@ -601,14 +690,21 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
 
             // ---- select the nearest unexpanded entry (and predict the one after it)
             int j = -1, j2 = -1;
+            uint64_t ku = 0, kn = KEY_NONE;   // their keys, taken from the lanes that read them
             for (uint32_t b0 = scan_from; b0 < len; b0 += 64) {
-                uint32_t i = b0 + lane;
-                bool un = (i < len) && !(beam[i] & 1ull);
-                uint64_t mk = __ballot(un);
+                const uint32_t i = b0 + lane;
+                const uint64_t bk = i < len ? beam[i] : 1ull;
+                const uint64_t mk = __ballot(!(bk & 1ull));
                 if (mk) {
-                    j = (int)(b0 + __ffsll((unsigned long long)mk) - 1);
-                    uint64_t rest = mk & (mk - 1ull);
-                    if (rest) j2 = (int)(b0 + __ffsll((unsigned long long)rest) - 1);
+                    const int l1 = __ffsll((unsigned long long)mk) - 1;
+                    j = (int)b0 + l1;
+                    ku = readlane64(bk, l1);
+                    const uint64_t rest = mk & (mk - 1ull);
+                    if (rest) {
+                        const int l2 = __ffsll((unsigned long long)rest) - 1;
+                        j2 = (int)b0 + l2;
+                        kn = readlane64(bk, l2);
+                    }
                     break;
                 }
             }
@@ -616,8 +712,6 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             PROF_T(t_sel1);
             PROF_ADD(0, t_sel1 - t_sel0);
             expanded_j = j;
-            const uint64_t ku = beam[j];
-            const uint64_t kn = j2 >= 0 ? beam[j2] : KEY_NONE;
             wave_sync();
             if (lane == 0) beam[j] = ku | 1ull;
             const uint32_t u = key_id(ku);
@@ -639,15 +733,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             PROF_ADD(12, t_row - t_sel1);
 
             // ---- test-and-insert into the visited set
-            int vst = 0;
-            if (v != BOA_PAD) vst = visit_lds(vs, v);
-            if (__ballot(vst < 0) != 0ull) {
-                if (!spill) {          // first overflow of this query: reset the bitmap
-                    spill = true;
-                    clear_bits(vs, lane);
-                }
-                if (vst < 0) vst = visit_bits(vs, v) ? 1 : 0;
-            }
+            const int vst = visit_test(v);
             PROF_T(t_vl);
             PROF_ADD(13, t_vl - t_row);
             const bool is_new = vst > 0;
