@@ -70,6 +70,7 @@ int ilog2(uint32_t x)
 struct PhasePlan {
     int32_t L;
     int32_t h_slots, wpb, blocks, lds_per_wave;
+    int32_t vis_bitmap;  // visited set as an LDS bitmap over all ids (0: hashed table)
     int32_t launches;
     int64_t capacity;   // waves resident at once on the whole GPU
     bool wide;          // scorer variant with twice the rows in flight
@@ -81,6 +82,7 @@ struct boa_index {
     int device = 0;
     int num_cu = 0;
     size_t lds_per_block_max = 65536;
+    size_t lds_per_block_hw = 65536;   // the device's own limit (bitmap escalations only)
     int vec_dtype = 0;
     IndexView view{};
     void *d_vectors = nullptr;
@@ -225,6 +227,7 @@ int boa_build_index_from_arrays(const void *vectors, int64_t n, int32_t d, int32
     }
     ix->num_cu = prop.multiProcessorCount;
     ix->lds_per_block_max = std::min<size_t>(prop.sharedMemPerBlock, 65536);
+    ix->lds_per_block_hw = prop.sharedMemPerBlock;
     ix->vec_dtype = vec_dtype;
 
     const int m_pad = m <= 1 ? 1 : (m <= 2 ? 2 : (m <= 4 ? 4 : 8));
@@ -472,9 +475,37 @@ PhasePlan plan_phase_widest(const boa_index *ix, int32_t L, int32_t forced_h, in
 // first. Widest visited table (fewest spills to the HBM bitmap) whose LDS
 // footprint still lets all S waves be resident at once; the default table
 // when even that is not possible.
+// The same launch with the visited set as an LDS bitmap over all n ids (one
+// wave per block): an exact set tested by a single LDS atomic, for indexes
+// small enough (n/8 bytes plus the worklist within the device's per-block
+// LDS) and survivor counts that it still lets be resident at once.
+PhasePlan plan_bitmap(const boa_index *ix, int32_t L, int64_t S)
+{
+    PhasePlan pl{};
+    pl.L = L;
+    pl.wide = true;
+    pl.vis_bitmap = 1;
+    pl.h_slots = 0;
+    const int64_t words = ((ix->view.n + 31) / 32 + 3) & ~(int64_t)3;
+    const int32_t Lb = (L + 1) & ~1, pw = ((L >> 6) + 3) & ~1;
+    const int64_t lds = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + 4 * words;
+    pl.lds_per_wave = (int32_t)((lds + 15) & ~(int64_t)15);
+    pl.wpb = 1;
+    if ((size_t)pl.lds_per_wave > ix->lds_per_block_hw) return pl;   // capacity 0: not possible
+    const int occ = phase_occupancy(ix->vec_dtype, ix->view.d, 1, (size_t)pl.lds_per_wave, true);
+    const int64_t blocks = (int64_t)std::max(occ, 0) * ix->num_cu;
+    pl.capacity = blocks;
+    pl.blocks = (int32_t)std::min<int64_t>(blocks, std::max<int64_t>(S, 1));
+    return pl;
+}
+
 PhasePlan plan_escalation(const boa_index *ix, int32_t L, int64_t S, int32_t forced_h)
 {
     if (forced_h > 0) return plan_phase(ix, L, forced_h, S, true);
+    {
+        PhasePlan bm = plan_bitmap(ix, L, S);
+        if (bm.capacity >= S) return bm;
+    }
     PhasePlan dflt = plan_phase(ix, L, 0, S, true);
     for (uint32_t h = 16384; h > (uint32_t)dflt.h_slots; h >>= 1) {
         PhasePlan pl = plan_phase(ix, L, (int32_t)h, S, true);
@@ -652,7 +683,7 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
             HIP_TRY(hipStreamSynchronize(st));
             if (S > 0) {
                 PhasePlan pe = plan_escalation(ix, sched.back(), S, p->lds_hash_slots);
-                if ((size_t)pe.lds_per_wave > ix->lds_per_block_max)
+                if ((size_t)pe.lds_per_wave > (pe.vis_bitmap ? ix->lds_per_block_hw : ix->lds_per_block_max))
                     return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
                 if ((uint64_t)pe.blocks * pe.wpb > slots)
                     return fail(BOA_EINVAL, "internal: escalation grid exceeds the spill bitmaps");
@@ -665,7 +696,9 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
                 e.p_begin = 1;
                 e.p_end = n_phases;
                 e.L_alloc = sched.back();
-                e.h_log2 = ilog2((uint32_t)pe.h_slots);
+                e.h_log2 = pe.vis_bitmap ? 3 : ilog2((uint32_t)pe.h_slots);   // (unused with the bitmap)
+                e.vis_bitmap = pe.vis_bitmap;
+                e.vis_words = pe.vis_bitmap ? (uint32_t)(((ix->view.n + 31) / 32 + 3) & ~(int64_t)3) : 0u;
                 e.lds_per_wave = pe.lds_per_wave;
                 e.waves_per_block = pe.wpb;
                 e.slot_base = 0;

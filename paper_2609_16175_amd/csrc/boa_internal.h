@@ -51,6 +51,8 @@ struct PhaseArgs {
     int32_t write_conf;       // record each query's confidence for a compaction/append
     int32_t L_alloc;          // widest of them: sizes the per-wave LDS
     int32_t h_log2;           // log2 of the LDS visited-table slots (16-bit entries)
+    int32_t vis_bitmap;       // 1: the visited set is instead an LDS bitmap over all n ids
+    uint32_t vis_words;       // its size in 32-bit words (a multiple of 4)
     uint32_t id_bits;         // bits of the largest id (ceil(log2 n))
     int32_t lds_per_wave, waves_per_block;
     uint32_t slot_base;

@@ -484,7 +484,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     vs.words32 = a.bits_words;
     vs.bits = a.bits + (size_t)slot * a.bits_words;
     vs.status = a.status;
-    const uint32_t table_words = (1u << a.h_log2) >> 1;
+    const uint32_t table_words = a.vis_bitmap ? a.vis_words : (1u << a.h_log2) >> 1;
 
     Scorer sc;
     // one point's attribute record (m_pad cells) and its violation count
@@ -550,6 +550,11 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         bool spill = false;
         // test-and-insert of this lane's neighbour: 1 new, 0 seen (or padding)
         auto visit_test = [&](uint32_t v) -> int {
+            if (a.vis_bitmap) {   // one bit per id: a single LDS atomic
+                if (v == BOA_PAD) return 0;
+                const uint32_t bit = 1u << (v & 31u);
+                return (atomicOr(&htab[v >> 5], bit) & bit) ? 0 : 1;
+            }
             int vst = 0;
             if (v != BOA_PAD) vst = visit_lds(vs, v);
             if (__ballot(vst < 0) != 0ull) {
@@ -572,7 +577,8 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         // the entry point is scored and entered before the first expansion
         uint32_t c = 1;
         if (lane == 0) {
-            visit_lds(vs, ix.entry);
+            if (a.vis_bitmap) htab[ix.entry >> 5] |= 1u << (ix.entry & 31u);
+            else visit_lds(vs, ix.entry);
             cid[0] = ix.entry;
         }
 
