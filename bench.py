@@ -390,6 +390,7 @@ def main():
         "operating_points": sweep,
         "fixed_L500": fixed,
         "speedup_vs_fixed_L500": round(qps / fixed["qps"], 3) if fixed else None,
+        "gathered_GBps_whole_search": round(gathered_bytes(st) * args.steps / (st["cum_kernel_ms"] * 1e-3) / 1e9, 1),
         "roofline": {"bound": "hbm", "kernel": KERNEL, "mode": mode, "phases": dom["phases"],
                      "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
