@@ -125,6 +125,27 @@ def recorded_traffic(workload: str):
         return None
 
 
+def cpu_model() -> str:
+    """Host CPU model name and socket count (from /proc/cpuinfo)."""
+    try:
+        txt = open("/proc/cpuinfo").read()
+        names = [l.split(":", 1)[1].strip() for l in txt.splitlines() if l.startswith("model name")]
+        sockets = {l.split(":", 1)[1].strip() for l in txt.splitlines() if l.startswith("physical id")}
+        return f"{names[0]} x {max(1, len(sockets))} socket(s)" if names else platform.machine()
+    except OSError:
+        return platform.machine()
+
+
+def doubling_widths(L0: int, Lmax: int) -> list:
+    """The widths L0, 2 L0, ... up to Lmax (the alpha = 2 schedule)."""
+    out, L = [], L0
+    while True:
+        out.append(L)
+        if L >= Lmax:
+            return out
+        L = min(2 * L, Lmax)
+
+
 def gathered_bytes(stats) -> float:
     return float(sum(p["gathered_bytes"] for p in stats["phases"]))
 
@@ -150,6 +171,7 @@ def main():
     ap.add_argument("--recall-target", type=float, default=0.95)
     ap.add_argument("--fixed-steps", type=int, default=3)
     ap.add_argument("--no-fixed", action="store_true")
+    ap.add_argument("--no-lneeded", action="store_true", help="skip the per-query 'L needed' analysis")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle timing")
     ap.add_argument("--lds-slots", type=int, default=0, help="force the LDS visited-table size")
@@ -324,6 +346,27 @@ def main():
         f"{dom['launches']} launches, {bytes_launch / 1e6:.2f} MB/launch -> {achieved:.1f} GB/s; "
         f"kernel time share {kernel_share:.2f}; groups {groups}")
 
+    # "L needed" (the paper's motivation figure): per query, the narrowest
+    # width of the alpha = 2 schedule whose fixed-width search already
+    # returns its exact filtered top-k; set against the width the adaptive
+    # search stopped at, it shows what the confidence test decides well
+    # (stopped early enough and right) and badly (stopped too early: lost)
+    lneed = None
+    if not args.no_lneeded:
+        widths = doubling_widths(wl.L0, wl.Lmax)
+        need = np.full(wl.nq, np.iinfo(np.int32).max, dtype=np.int64)
+        for Lw in reversed(widths):
+            o = index.search(q, r, k=wl.k, fixed_L=Lw)
+            rq_w = recall(o.ids.cpu().numpy().view(np.uint32), o.dists.cpu().numpy(), gt_ids, gt_d, n_valid,
+                          wl.k, per_query=True)
+            need[rq_w >= 1.0 - 1e-9] = Lw
+        lneed = {"widths": widths,
+                 "pct_by_L_needed": {str(Lw): round(100.0 * float((need == Lw).mean()), 2) for Lw in widths},
+                 "pct_beyond_Lmax": round(100.0 * float((need > wl.Lmax).mean()), 2),
+                 "pct_stopped_below_L_needed": round(100.0 * float((final_L < need).mean()), 2),
+                 "pct_escalated_past_L_needed": round(100.0 * float((final_L > need).mean()), 2)}
+        log(f"L needed: {lneed}")
+
     fixed = None
     if not args.no_fixed:
         msf, stf, out_f = timed(dict(k=wl.k, fixed_L=500), args.fixed_steps, 1)
@@ -350,10 +393,16 @@ def main():
         ref = oracle.boa(oix, data.queries[:ns], data.ranges[:ns], wl.k, osched, eps=chosen["eps"], threads=threads)
         el = time.perf_counter() - tc
         same = int(((ref.ids == ids[:ns]).all(1) & (ref.final_L == final_L[:ns])).sum())
+        # the oracle on one thread as well (a smaller sample of the same queries)
+        n1 = int(min(ns, max(1, (args.cpu_seconds / 3.0) / max(el * threads / ns, 1e-6))))
+        tc = time.perf_counter()
+        oracle.boa(oix, data.queries[:n1], data.ranges[:n1], wl.k, osched, eps=chosen["eps"], threads=1)
+        el1 = time.perf_counter() - tc
         cpu = dict(value=round(ns / el, 2), unit="queries/s", cores=threads, kind="oracle",
                    sample=f"first {ns} of {wl.nq} queries, full adaptive schedule, {threads} threads, "
                           f"{el:.1f}s wall",
-                   cpu_model=platform.processor() or platform.machine(),
+                   one_thread_value=round(n1 / el1, 2), one_thread_sample=f"first {n1} queries, {el1:.1f}s wall",
+                   cpu_model=cpu_model(),
                    gpu_identical_on_sample=f"{same}/{ns}")
         log(f"cpu oracle: {cpu['value']:.1f} QPS on {ns} queries x {threads} threads; "
             f"GPU identical on {same}/{ns}")
@@ -385,6 +434,7 @@ def main():
         "recall_by_final_L": rec_by_L,
         "phases": [{k2: (round(v, 4) if isinstance(v, float) else v) for k2, v in p.items()}
                    for p in st["phases"]],
+        "L_needed": lneed,
         "recall_target": args.recall_target,
         "recall_target_met": target_met,
         "operating_points": sweep,

@@ -116,6 +116,22 @@ def test_forced_spill_changes_nothing(tiny, slots, mode):
     assert_parity(got, ref, f"spill slots={slots}, repeated")
 
 
+@pytest.mark.parametrize("eps", [0.0, 0.005, 0.05])
+def test_split_escalation_bitmap_and_table(tiny, eps):
+    """The split search's escalation launch keeps its visited set as an LDS
+    bitmap over all ids when that fits (10k points: 1.25 KB) and as the
+    hashed table when a table size is forced; both are exact sets, so both
+    equal the oracle, with almost every query escalating at small eps."""
+    wl, d = tiny["wl"], tiny["data"]
+    sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
+    ref = oracle.boa(tiny["orc"], d.queries, d.ranges, wl.k, sched, eps=eps)
+    assert ref.phases[1]["active"] > 0
+    for slots in (0, 4096):
+        got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax, eps=eps,
+                         split=True, lds_hash_slots=slots)
+        assert_parity(got, ref, f"split eps={eps} slots={slots}")
+
+
 @pytest.mark.parametrize("mode", list(MODES))
 def test_paper_schedule(tiny, mode):
     """The paper's experiments use widths 10, 100, 200 (Sec. IV)."""
