@@ -5,10 +5,10 @@
 // (Alg. 2, one node per iteration):
 //   1. select the first not-yet-expanded worklist entry (ballot scan);
 //   2. gather its adjacency row, one neighbour per lane (one coalesced load);
-//   3. test-and-insert every neighbour into the query's visited set: an
-//      open-addressing table in LDS that spills, once its load passes one
-//      half, into a per-wave bitmap over all points in HBM (one atomic OR
-//      per neighbour);
+//   3. test-and-insert every neighbour into the query's visited set: a
+//      two-choice bucketed table of 16-bit entries in LDS whose overflow
+//      goes to a per-wave bitmap over all points in HBM, or (the escalation
+//      launch of a split search, when it fits) an LDS bitmap over all ids;
 //   4. for the unseen neighbours: gather the attribute cells and count the
 //      violated range predicates (phi, Eq. 2), gather the vector and compute
 //      the squared L2 distance with a 16-lane (float32) or G-lane (uint8)
@@ -16,7 +16,8 @@
 //   5. pack (phi, distance, id) into one 64-bit key, drop keys that cannot
 //      enter the worklist, sort the rest by counting (each key's rank is the
 //      number of survivors below it), and merge them into the sorted
-//      worklist held in LDS: each new key's rank by binary search, its
+//      worklist held in LDS: each new key's rank by binary search (eight-
+//      way in the escalation variant), its
 //      output slot marked in a bitmap, and the suffix rebuilt backwards in
 //      64-entry chunks where a popcount of the bitmap tells every output
 //      slot where its entry comes from.
@@ -83,8 +84,6 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-__device__ __forceinline__ uint32_t hash32(uint32_t v) { return v * 0x9E3779B1u; }
-
 // first index i in [0, n) with a[i] >= key (a sorted ascending)
 __device__ __forceinline__ uint32_t lower_bound64(const uint64_t *a, uint32_t n, uint64_t key)
 {
@@ -117,16 +116,6 @@ __device__ __forceinline__ uint32_t lower_bound64_8way(const uint64_t *a, uint32
     }
     return lo;
 }
-// number of entries of a[0, n) that are <= x (a sorted ascending)
-__device__ __forceinline__ uint32_t upper_bound32(const uint32_t *a, uint32_t n, uint32_t x)
-{
-    uint32_t lo = 0, hi = n;
-    while (lo < hi) {
-        uint32_t mid = (lo + hi) >> 1;
-        if (a[mid] <= x) lo = mid + 1; else hi = mid;
-    }
-    return lo;
-}
 
 // Cross-lane move inside a 16-lane row by DPP (no LDS round trip):
 // row_shr:J gives lane i the value of lane i-J; lanes whose source falls
@@ -151,7 +140,6 @@ __device__ __forceinline__ float from_lane_minus_f(float v)
 template <int T, int W = 1>
 struct F32Scorer {
     // lane p = lane & 15 accumulates float4 chunks p, p+16, p+32, ...
-    static constexpr int kGroup = 16;
     static constexpr bool kWide = W == 2;
     float4 q[T];
 
@@ -255,7 +243,6 @@ template <int G, int W = 1>
 struct U8Scorer {
     // lane p = lane % G holds the query's 16-byte chunk p (p < d/16); the
     // exact int32 sum is order-free.
-    static constexpr int kGroup = G;
     static constexpr bool kWide = W == 2;
     uint4 q;
 
