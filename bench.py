@@ -320,6 +320,28 @@ def main():
     log(f"recall@10 {rec_tie:.4f} (strict {rec_strict:.4f}); L_avg {L_avg:.1f}; split {split}; "
         f"recall by final L {rec_by_L}")
 
+    # the same search with its host transfers inside the timed loop: queries
+    # and ranges copied from pinned host memory to HBM, the results copied
+    # back (a caller whose queries arrive over PCIe); not the headline value,
+    # which has the inputs resident in HBM
+    qh, rh = torch.from_numpy(data.queries).pin_memory(), torch.from_numpy(data.ranges).pin_memory()
+    hosts = [torch.empty(t.shape, dtype=t.dtype).pin_memory() for t in (out.ids, out.dists, out.final_L)]
+    e2e_kw = dict(kw, **mode_kw[mode])
+    for it in range(args.warmup + args.steps):
+        if it == args.warmup:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+        o_h = index.search(qh.to(dev, non_blocking=True), rh.to(dev, non_blocking=True), **e2e_kw)
+        for h, t_dev in zip(hosts, (o_h.ids, o_h.dists, o_h.final_L)):
+            h.copy_(t_dev, non_blocking=True)
+        torch.cuda.synchronize()
+    ms_e2e = (time.perf_counter() - t0) * 1e3 / args.steps
+    assert np.array_equal(hosts[0].numpy().view(np.uint32), ids), "end-to-end results differ"
+    e2e = dict(mode=mode, ms_per_step=round(ms_e2e, 4), qps=round(wl.nq / (ms_e2e / 1e3), 1),
+               host_bytes_per_step=int(qh.numel() * qh.element_size() + rh.numel() * rh.element_size()
+                                       + sum(h.numel() * h.element_size() for h in hosts)))
+    log(f"end to end with host transfers ({mode}): {ms_e2e:.3f} ms/step, {e2e['qps']:,.0f} QPS")
+
     # roofline of the dominant kernel: launches are grouped by the phase they
     # start at (a split search has two kernels: the first phase, and the
     # escalation through every later phase); each group's algorithmic bytes
@@ -441,6 +463,7 @@ def main():
         "fixed_L500": fixed,
         "speedup_vs_fixed_L500": round(qps / fixed["qps"], 3) if fixed else None,
         "gathered_GBps_whole_search": round(gathered_bytes(st) * args.steps / (st["cum_kernel_ms"] * 1e-3) / 1e9, 1),
+        "end_to_end_with_host_transfers": e2e,
         "roofline": {"bound": "hbm", "kernel": KERNEL, "mode": mode, "phases": dom["phases"],
                      "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
