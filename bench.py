@@ -166,7 +166,7 @@ def main():
                     help="confidence threshold of Eq. 3; 0: choose from --eps-grid (see --alpha)")
     ap.add_argument("--alpha", type=float, default=0.0,
                     help="growth factor of the width schedule; 0: choose from --alpha-grid")
-    ap.add_argument("--eps-grid", default="0.005,0.01,0.02,0.05,0.1,0.15,0.2")
+    ap.add_argument("--eps-grid", default="0,0.001,0.005,0.01,0.02,0.05,0.1,0.15,0.2")
     ap.add_argument("--alpha-grid", default="2,32")
     ap.add_argument("--recall-target", type=float, default=0.95)
     ap.add_argument("--fixed-steps", type=int, default=3)
