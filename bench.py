@@ -6,8 +6,9 @@ the workload, with the index, queries and ranges resident in HBM. Prints
 one JSON line: filtered QPS, recall@10 against exhaustive filtered search,
 average final beamwidth, the fixed-width (L=500) baseline built from the
 same kernel, the roofline position of the search kernel (algorithmic
-gathered bytes over the kernel's HIP-event time), and the CPU oracle timed
-on the host cores.
+gathered bytes over the kernel's HIP-event time), the same search with its
+host transfers inside the timed loop (queries in, results out; reported
+beside the value, never as it), and the CPU oracle timed on the host cores.
 
 The graph is built in-process by the workloads package (exact kNN on the
 GPU with torch matmul, then pruning and a navigation layer); that is input
@@ -184,6 +185,8 @@ def main():
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
+    if args.steps < 1 or args.warmup < 0:
+        ap.error("--steps must be >= 1 and --warmup >= 0")
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
