@@ -126,6 +126,30 @@ def recorded_traffic(workload: str):
         return None
 
 
+SEL_EDGES = (0.0, 1e-4, 1e-3, 1e-2, 0.03, 0.1, 0.3, 1.0)
+
+
+def selectivity_summary(n_valid, n: int, k: int, per_query_recall=None) -> dict:
+    """Realised joint selectivity of the query ranges (|D_f| / n per query,
+    from the exhaustive pass): quantiles, a histogram over fixed bins, the
+    queries with fewer than k valid points, and (given per-query recall)
+    the mean recall of each bin."""
+    nv = np.asarray(n_valid, dtype=np.int64)
+    sel = nv.astype(np.float64) / n
+    counts, _ = np.histogram(sel, bins=SEL_EDGES)
+    label = [f"{lo:g}-{hi:g}" for lo, hi in zip(SEL_EDGES[:-1], SEL_EDGES[1:])]
+    out = {"median": round(float(np.median(sel)), 6), "p5": round(float(np.percentile(sel, 5)), 6),
+           "p95": round(float(np.percentile(sel, 95)), 6), "min_valid_points": int(nv.min()),
+           "queries_with_fewer_than_k": int((nv < k).sum()),
+           "histogram": {lb: int(c) for lb, c in zip(label, counts)}}
+    if per_query_recall is not None:
+        rq = np.asarray(per_query_recall, dtype=np.float64)
+        b = np.clip(np.searchsorted(SEL_EDGES, sel, side="right") - 1, 0, len(label) - 1)
+        out["recall_by_bin"] = {label[i]: round(float(rq[b == i].mean()), 4)
+                                for i in range(len(label)) if (b == i).any()}
+    return out
+
+
 def cpu_model() -> str:
     """Host CPU model name and socket count (from /proc/cpuinfo)."""
     try:
@@ -457,6 +481,7 @@ def main():
         "L_work": round(L_work, 2),
         "phase_split_pct": split,
         "recall_by_final_L": rec_by_L,
+        "selectivity": selectivity_summary(n_valid, wl.n, wl.k, rq),
         "phases": [{k2: (round(v, 4) if isinstance(v, float) else v) for k2, v in p.items()}
                    for p in st["phases"]],
         "L_needed": lneed,

@@ -39,3 +39,20 @@ def test_recorded_traffic_follows_the_source_digest(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     monkeypatch.setattr(bench, "source_digest", lambda: "f" * 64)
     assert bench.recorded_traffic(key) is None
+
+
+def test_selectivity_summary():
+    import numpy as np
+    n, k = 1000, 10
+    n_valid = np.array([0, 5, 10, 50, 500, 1000], dtype=np.int64)
+    rq = np.array([1.0, 0.5, 1.0, 0.8, 0.9, 1.0])
+    s = bench.selectivity_summary(n_valid, n, k, rq)
+    assert s["min_valid_points"] == 0 and s["queries_with_fewer_than_k"] == 2
+    assert sum(s["histogram"].values()) == len(n_valid)
+    # 0 -> first bin; 0.005 and 0.01 -> [1e-3, 1e-2) and [1e-2, 0.03); 1.0 -> last bin
+    assert s["histogram"]["0-0.0001"] == 1
+    assert s["histogram"]["0.001-0.01"] == 1
+    assert s["histogram"]["0.01-0.03"] == 1
+    assert s["histogram"]["0.3-1"] == 2
+    assert s["recall_by_bin"]["0.3-1"] == 0.95
+    assert abs(s["median"] - 0.03) < 1e-12
