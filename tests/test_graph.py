@@ -128,3 +128,56 @@ def test_ivf_candidates_probing_few_lists():
         assert (A[rows[fin], cl[li][fin]] <= thr[rows[fin], li]).all()
         assert (cl[li][fin] != rows[fin]).all()
         assert (dl[li][:, 1:] >= dl[li][:, :-1]).all()
+
+
+def test_subset_level_candidates_match_brute_force():
+    # random-subset levels: each point's nearest members of a seeded subset
+    # (itself excluded), after the attribute levels, sorted by (distance, id)
+    x, a = _small(n=600, d=8)
+    n = x.shape[0]
+    X = torch.from_numpy(x).double()
+    QA = torch.from_numpy(graph.attribute_quantiles(a, [0, 0]))
+    thr = graph._thresholds(QA, (0.1,), seed=1, chunk=128)
+    g = np.random.default_rng(9)
+    member = torch.from_numpy(g.random((2, n)) < np.array([[0.05], [0.3]]))
+    du, cand, du_l, cand_l = graph.candidates(X, 8, QA, thr, 5, chunk=128, member=member)
+    assert du_l.shape == (3, n, 5)
+    xd = x.astype(np.float64)
+    D = ((xd[:, None, :] - xd[None, :, :]) ** 2).sum(-1)
+    np.fill_diagonal(D, np.inf)
+    for i in range(0, n, 29):
+        for s in range(2):
+            Dm = np.where(member[s].numpy()[None, :], D[i][None, :], np.inf)[0]
+            o = np.lexsort((np.arange(n), Dm))[:5]
+            fin = np.isfinite(Dm[o])
+            got = cand_l[1 + s, i][torch.from_numpy(fin)].tolist()
+            assert got == o[fin].tolist()
+            assert np.array_equal(np.isfinite(du_l[1 + s, i].numpy()), fin)
+            assert all(member[s, j] and j != i for j in got)
+
+
+def test_ivf_subset_levels_with_every_list_probed_are_exact():
+    x, a = _clustered(n=2000)
+    n = x.shape[0]
+    X = torch.from_numpy(x).double()
+    member = torch.from_numpy(np.random.default_rng(4).random((2, n)) < np.array([[0.02], [0.2]]))
+    ref = graph.candidates(X, 10, None, None, 6, chunk=512, member=member)
+    got = graph.candidates_ivf(X, 10, None, None, 6, lists=12, nprobe=12, batch_elems=1 << 22, member=member)
+    fin = torch.isfinite(ref[2])
+    assert torch.equal(fin, torch.isfinite(got[2]))
+    assert torch.equal(torch.where(fin, ref[3], -1), torch.where(fin, got[3], -1))
+    assert torch.allclose(ref[2][fin], got[2][fin], rtol=1e-12, atol=1e-9)
+
+
+def test_graph_rows_hold_subset_and_navigation_edges():
+    # with subset levels and the default budgets every row stays within R,
+    # is duplicate- and self-free, and the graph is reachable from the entry
+    x, a = _clustered(n=2500, d=16, k=20)
+    R = 32
+    adj, entry = graph.build_graph(x, R, "cpu", attrs=a, attr_dtypes=[0, 0], sub_levels=(0.01, 0.1))
+    n = x.shape[0]
+    assert adj.shape == (n, R)
+    for i in range(0, n, 7):
+        row = adj[i][adj[i] != graph.PAD].astype(np.int64)
+        assert i not in row and len(set(row.tolist())) == len(row) and (row < n).all()
+    assert graph._reachable(n, adj, entry).all()
