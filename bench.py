@@ -90,7 +90,10 @@ def recall(ids, dists, gt_ids, gt_d, n_valid, k, per_query=False):
     for i in range(len(ids)):
         f = ids[i][ids[i] != 0xFFFFFFFF]
         g = gt_ids[i][np.isfinite(gt_d[i])]
-        strict[i] = len(set(f.tolist()) & set(g.tolist())) / denom[i]
+        if len(g):
+            strict[i] = len(set(f.tolist()) & set(g.tolist())) / denom[i]
+        else:   # no valid point: returning nothing is the whole answer
+            strict[i] = 1.0 if len(f) == 0 else 0.0
         if len(g):
             dk = gt_d[i][len(g) - 1]
             fd = dists[i][:len(f)].astype(np.float64)

@@ -56,3 +56,61 @@ def test_selectivity_summary():
     assert s["histogram"]["0.3-1"] == 2
     assert s["recall_by_bin"]["0.3-1"] == 0.95
     assert abs(s["median"] - 0.03) < 1e-12
+
+
+def test_recall_strict_and_tie_tolerant():
+    import numpy as np
+    PAD = 0xFFFFFFFF
+    k = 3
+    gt_ids = np.array([[1, 2, 3], [5, 6, -1], [0, 0, 0]], dtype=np.int64)
+    gt_d = np.array([[1.0, 2.0, 3.0], [1.0, 4.0, np.inf], [np.inf, np.inf, np.inf]])
+    n_valid = np.array([10, 2, 0])
+    # query 0: ids 1, 2 right, 9 wrong but tied with the 3rd exact distance
+    # query 1: both valid points found, then padding
+    # query 2: no valid point, nothing returned
+    ids = np.array([[1, 2, 9], [6, 5, PAD], [PAD, PAD, PAD]], dtype=np.uint32)
+    dists = np.array([[1.0, 2.0, 3.0], [4.0, 1.0, np.inf], [np.inf, np.inf, np.inf]], dtype=np.float32)
+    strict, tie = bench.recall(ids, dists, gt_ids, gt_d, n_valid, k)
+    per_q = bench.recall(ids, dists, gt_ids, gt_d, n_valid, k, per_query=True)
+    assert abs(strict - (2 / 3 + 1 + 1) / 3) < 1e-12
+    np.testing.assert_allclose(per_q, [1.0, 1.0, 1.0])
+    assert abs(tie - 1.0) < 1e-12
+    # a farther wrong id is not forgiven
+    ids2 = ids.copy()
+    dists2 = dists.copy()
+    dists2[0, 2] = 3.5
+    per_q2 = bench.recall(ids2, dists2, gt_ids, gt_d, n_valid, k, per_query=True)
+    assert abs(per_q2[0] - 2 / 3) < 1e-12
+
+
+def test_exact_filtered_topk_matches_brute_force():
+    import numpy as np
+    import torch
+    from workloads import gen
+    g = np.random.default_rng(7)
+    n, d, nq, k = 400, 12, 20, 5
+    X = g.normal(size=(n, d)).astype(np.float32)
+    Q = g.normal(size=(nq, d)).astype(np.float32)
+    A = np.empty((n, 2), dtype=np.int32)
+    A[:, 0] = g.integers(0, 100, size=n)
+    A[:, 1] = gen.f32_bits(g.normal(size=n).astype(np.float32))
+    R = np.empty((nq, 2, 2), dtype=np.int32)
+    lo = g.integers(0, 60, size=nq)
+    R[:, 0, 0], R[:, 0, 1] = lo, lo + g.integers(0, 40, size=nq)
+    fl = np.sort(g.normal(size=(nq, 2)).astype(np.float32), axis=1)
+    R[:, 1, 0], R[:, 1, 1] = gen.f32_bits(fl[:, 0]), gen.f32_bits(fl[:, 1])
+    R[0, 0] = [1000, 2000]   # no valid point
+    ids, dd, nv = bench.exact_filtered_topk(torch, torch.from_numpy(X), torch.from_numpy(A), {1},
+                                            torch.from_numpy(Q), torch.from_numpy(R), k, chunk=7)
+    a1 = gen.cells_as_f32(A[:, 1])
+    for i in range(nq):
+        lo1, hi1 = gen.cells_as_f32(R[i, 1])
+        ok = (A[:, 0] >= R[i, 0, 0]) & (A[:, 0] <= R[i, 0, 1]) & (a1 >= lo1) & (a1 <= hi1)
+        assert nv[i] == ok.sum()
+        dist = ((X.astype(np.float64) - Q[i].astype(np.float64)) ** 2).sum(1)
+        dist[~ok] = np.inf
+        o = np.lexsort((np.arange(n), dist))[:k]
+        fin = np.isfinite(dist[o])
+        assert ids[i][fin].tolist() == o[fin].tolist()
+        np.testing.assert_allclose(dd[i][fin], dist[o][fin], rtol=1e-12)
+        assert np.isinf(dd[i][~fin]).all()
