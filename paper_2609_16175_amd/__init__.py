@@ -3,9 +3,9 @@ adaptation ("BOA: Beamwidth Online Adaptation for Filtered-ANNS on a GPU").
 
 Thin ctypes binding of libboa.so (include/boa.h): argument marshalling
 only. Every step of the search runs in the library's HIP kernels; torch
-provides device memory and the stream. Importing this package on a
-machine where libboa.so is not built raises, loudly: there is no CPU
-fallback.
+provides device memory and the stream. The library is loaded on first
+use; where libboa.so is not built, that first use raises ImportError:
+there is no CPU fallback.
 """
 from __future__ import annotations
 

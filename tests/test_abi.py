@@ -86,3 +86,16 @@ def test_search_null_index():
     p = boa.default_params()
     rc = boa.lib().boa_search(None, None, None, 0, C.byref(p), None, None, None, None, None, None)
     assert rc == -1
+
+
+def test_missing_library_fails_loudly():
+    # no fallback: with the library absent, the binding refuses to run
+    import subprocess
+    import sys
+    code = ("import paper_2609_16175_amd as boa\n"
+            "try:\n    boa.lib()\nexcept ImportError as e:\n    print('refused:', e)\n"
+            "else:\n    print('loaded')\n")
+    env = dict(os.environ, BOA_LIB="libboa_missing_for_test.so")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env,
+                       cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))), timeout=120)
+    assert "refused:" in r.stdout and "is not built" in r.stdout, r.stdout + r.stderr
