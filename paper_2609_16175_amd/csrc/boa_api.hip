@@ -315,10 +315,10 @@ int ensure_workspace(boa_index *ix, int64_t nq, int32_t n_phases, uint64_t slots
         ix->nq_cap = cap;
         ix->ph_cap = pc;
     }
-    if (!ix->n_active) {
-        if ((rc = dalloc(&ix->n_active, 2 * (BOA_MAX_PHASES + 1)))) return rc;
-        if ((rc = dalloc(&ix->status, 16))) return rc;
-    }
+    // each under its own check: a failed allocation of one is retried by the
+    // next search instead of leaving the other null
+    if (!ix->n_active && (rc = dalloc(&ix->n_active, 2 * (BOA_MAX_PHASES + 1)))) return rc;
+    if (!ix->status && (rc = dalloc(&ix->status, 16))) return rc;
     if (n_counters > ix->n_counters) {
         dfree(ix->counters);
         if ((rc = dalloc(&ix->counters, n_counters))) return rc;

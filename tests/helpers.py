@@ -102,3 +102,43 @@ def assert_same_up_to_near_ties(ids, dists, ref_ids, ref_d64, rel=1e-5):
             assert a in set(ref_ids[near]) or near.sum() > 1, (j, a, b)
 
 
+
+
+def load_beam_trace(path):
+    """The hand-traced golden graph of tests/golden/beam_trace.txt:
+    (vectors n x 4 float32, attrs n x 1, adjacency n x 3, entry, queries
+    {name: (q, ranges)}, SEARCH cases, BOA cases)."""
+    pts, adj, queries, searches, boas, entry = {}, {}, {}, [], [], None
+    with open(path) as f:
+        for line in f:
+            p = line.split()
+            if not p or p[0].startswith("#"):
+                continue
+            if p[0] == "POINT":
+                pts[int(p[1])] = (float(p[2]), float(p[3]), int(p[4]))
+            elif p[0] == "ADJ":
+                adj[int(p[1])] = [PAD if v == "-" else int(v) for v in p[2:]]
+            elif p[0] == "ENTRY":
+                entry = int(p[1])
+            elif p[0] == "QUERY":
+                queries[p[1]] = (np.array([[float(p[2]), float(p[3]), 0, 0]], dtype=np.float32),
+                                 np.array([[[int(p[4]), int(p[5])]]], dtype=np.int32))
+            elif p[0] == "SEARCH":
+                items = [tuple(int(t) for t in s.split("/")) for s in p[5:]]
+                searches.append(dict(q=p[1], L=int(p[2]), E=int(p[3]), S=int(p[4]),
+                                     ids=[a for a, _, _ in items], phi=[b for _, b, _ in items],
+                                     d=[c for _, _, c in items]))
+            elif p[0] == "BOA":
+                items = [tuple(int(t) for t in s.split("/")) for s in p[8:]]
+                boas.append(dict(q=p[1], k=int(p[2]), eps=float(p[3]),
+                                 widths=[int(w) for w in p[4].split(",")], final_L=int(p[5]),
+                                 E=int(p[6]), S=int(p[7]), ids=[a for a, _ in items],
+                                 d=[b for _, b in items]))
+    n = len(pts)
+    x = np.zeros((n, 4), dtype=np.float32)
+    a = np.zeros((n, 1), dtype=np.int32)
+    for i, (px, py, av) in pts.items():
+        x[i, :2] = (px, py)
+        a[i, 0] = av
+    A = np.array([adj[i] for i in range(n)], dtype=np.uint32)
+    return x, a, A, entry, queries, searches, boas

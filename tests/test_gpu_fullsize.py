@@ -1,9 +1,14 @@
 """GPU parity at the workloads' full sizes, in the benchmark's launch
 configuration: the whole 10,000-query batch runs on the GPU (fused, split, phased
-and BOA+ modes, and the fixed-width baseline); a seeded sample of queries is
-recomputed by the CPU oracle one by one and compared row by row. Because a
-query's result does not depend on the rest of the batch (every phase
-restarts the search), the oracle's sample is an exact check of those rows.
+and BOA+ modes, and the fixed-width baseline at L = 16, 500 and 512); a seeded
+sample of queries is recomputed by the CPU oracle one by one and compared row
+by row. Because a query's result does not depend on the rest of the batch
+(every phase restarts the search), the oracle's sample is an exact check of
+those rows. Every row of every batch is also checked against what holds at
+any size: each returned id satisfies all of its query's range predicates
+(Eq. 2, per column type), its reported distance is its squared distance to
+the query (recomputed in float64), rows ascend by (distance, id) with no
+repeated id, and padding only trails.
 """
 import numpy as np
 import pytest
@@ -42,6 +47,51 @@ def _rows(out, sel):
             out.expansions.cpu().numpy().astype(np.int64)[sel], out.scored.cpu().numpy().astype(np.int64)[sel])
 
 
+def check_whole_batch(out, data, wl, what):
+    """Properties of every row of a batch result (see the module docstring)."""
+    from workloads import gen
+    ids = out.ids.cpu().numpy().view(np.uint32)
+    dists = out.dists.cpu().numpy()
+    nq, k = ids.shape
+    assert (nq, k) == (wl.nq, wl.k), what
+    pad = ids == 0xFFFFFFFF
+    # padding only trails, with +inf distances
+    assert not (pad[:, :-1] & ~pad[:, 1:]).any(), f"{what}: padding before a result"
+    assert np.isinf(dists[pad]).all() and np.isfinite(dists[~pad]).all(), what
+    safe = np.where(pad, 0, ids).astype(np.int64)
+    assert (safe < wl.n).all(), f"{what}: id out of range"
+    # Eq. 2 for every returned id, column by column in its own type
+    a = data.attrs[safe]                     # nq x k x m
+    ok = np.ones((nq, k), dtype=bool)
+    for j, t in enumerate(wl.attr_dtypes):
+        lo, hi = data.ranges[:, j, 0][:, None], data.ranges[:, j, 1][:, None]
+        col = a[:, :, j]
+        if t == gen.ATTR_F32:
+            col, lo, hi = gen.cells_as_f32(col), gen.cells_as_f32(lo), gen.cells_as_f32(hi)
+        ok &= (lo <= col) & (col <= hi)
+    bad = np.flatnonzero((~ok & ~pad).any(1))
+    assert bad.size == 0, f"{what}: {bad.size} rows return an id violating its predicates (row {bad[:1]})"
+    # the reported distance is the id's squared distance (float64 recompute)
+    d64 = np.empty((nq, k), dtype=np.float64)
+    for s0 in range(0, nq, 1000):
+        x = data.vectors[safe[s0:s0 + 1000]].astype(np.float64)
+        q = data.queries[s0:s0 + 1000].astype(np.float64)[:, None, :]
+        d64[s0:s0 + 1000] = ((x - q) ** 2).sum(-1)
+    exact = wl.vec_dtype == gen.VEC_U8 or wl.name.startswith("sift-like")   # integer data
+    err = np.abs(dists.astype(np.float64) - d64)[~pad]
+    tol = 0.0 if exact else 1e-5
+    assert (err <= tol * np.maximum(d64[~pad], 1e-30) + (0 if exact else 1e-7)).all(), \
+        f"{what}: reported distance differs from the recomputed one by up to {err.max()}"
+    # ascending by (distance, id), no repeated id
+    d0, d1 = dists[:, :-1], dists[:, 1:]
+    i0, i1 = ids[:, :-1], ids[:, 1:]
+    both = ~pad[:, 1:]
+    order_ok = (d0 < d1) | ((d0 == d1) & (i0 < i1))
+    assert (order_ok | ~both).all(), f"{what}: a row is not ascending by (distance, id)"
+    srt = np.sort(np.where(pad, np.arange(k)[None, :] + (1 << 32), ids.astype(np.int64)), axis=1)
+    assert not (srt[:, 1:] == srt[:, :-1]).any(), f"{what}: a row repeats an id"
+
+
 def _check(got, ref, what):
     ids, dists, fl, E, S = got
     bad = np.flatnonzero((ids != ref.ids).any(1) | (dists != ref.dists).any(1) | (fl != ref.final_L)
@@ -69,23 +119,31 @@ def test_full_size_index_builds(full):
     assert graph._reachable(wl.n, adj, full["entry"]).all()
 
 
-def test_full_size_adaptive_sampled(full):
+MODES = ({"fused": True}, {"split": True}, {}, {"boa_plus": True, "sub_batches": 10})
+
+
+@pytest.mark.parametrize("eps,alpha", [(0.05, 2.0), (0.2, 32.0), (0.005, 32.0)])
+def test_full_size_adaptive_sampled(full, eps, alpha):
+    """Alg. 1 at the paper's point (eps 0.05, alpha 2) and at the two-step
+    schedules (16 then Lmax) the benchmark's operating points use."""
     wl, d, s = full["wl"], full["data"], full["sample"]
-    sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
-    ref = oracle.boa(full["orc"], d.queries[s], d.ranges[s], wl.k, sched, threads=16)
-    for mode in ({"fused": True}, {"split": True}, {}, {"boa_plus": True, "sub_batches": wl.sub_batches}):
-        out = full["gpu"].search(full["q"], full["r"], k=wl.k, L0=wl.L0, Lmax=wl.Lmax, counters=True, **mode)
+    sched = oracle.schedule(wl.L0, alpha, wl.Lmax)
+    ref = oracle.boa(full["orc"], d.queries[s], d.ranges[s], wl.k, sched, eps=eps, threads=16)
+    for mode in MODES:
+        out = full["gpu"].search(full["q"], full["r"], k=wl.k, L0=wl.L0, Lmax=wl.Lmax, eps=eps, alpha=alpha,
+                                 counters=True, **mode)
         torch.cuda.synchronize()
-        _check(_rows(out, s), ref, f"{wl.name} {mode or 'phased'}")
-        # every result id satisfies the predicates of its query (whole batch)
-        ids = out.ids.cpu().numpy().view(np.uint32)
-        assert ids.shape == (wl.nq, wl.k)
+        what = f"{wl.name} eps={eps} alpha={alpha} {mode or 'phased'}"
+        _check(_rows(out, s), ref, what)
+        check_whole_batch(out, d, wl, what)
 
 
-def test_full_size_fixed_width_sampled(full):
+@pytest.mark.parametrize("L", [16, 500, 512])
+def test_full_size_fixed_width_sampled(full, L):
     wl, d = full["wl"], full["data"]
     s = full["sample"][:SAMPLE_FIXED]
-    ref = oracle.boa(full["orc"], d.queries[s], d.ranges[s], wl.k, [500], threads=16)
-    out = full["gpu"].search(full["q"], full["r"], k=wl.k, fixed_L=500, counters=True)
+    ref = oracle.boa(full["orc"], d.queries[s], d.ranges[s], wl.k, [L], threads=16)
+    out = full["gpu"].search(full["q"], full["r"], k=wl.k, fixed_L=L, counters=True)
     torch.cuda.synchronize()
-    _check(_rows(out, s), ref, f"{wl.name} fixed L=500")
+    _check(_rows(out, s), ref, f"{wl.name} fixed L={L}")
+    check_whole_batch(out, d, wl, f"{wl.name} fixed L={L}")

@@ -277,3 +277,32 @@ def test_split_all_or_no_survivors(tiny, eps):
     assert (survivors == 0) == (eps == 1.0)
     assert st["phases"][0]["launches"] == 1
     assert st["phases"][1]["launches"] == (1 if survivors else 0)
+
+
+# ---------------------------------------------------------------------------
+# the hand-traced golden graph (tests/golden/beam_trace.txt): the kernel's
+# final results, widths and counts equal the values worked by hand
+
+def test_hand_traced_golden():
+    import os
+    from helpers import load_beam_trace
+    x, a, adj, entry, queries, searches, boas = load_beam_trace(
+        os.path.join(os.path.dirname(__file__), "golden", "beam_trace.txt"))
+    gpu = _boa().Index(x, a, np.zeros(1, np.int32), adj, entry)
+    for c in searches:
+        # single width: the valid entries of the traced worklist, in order
+        q, r = queries[c["q"]]
+        valid = [(i, d) for i, p, d in zip(c["ids"], c["phi"], c["d"]) if p == 0]
+        ids, dists, fl, E, S = gpu_search(gpu, q, r, k=len(valid), fixed_L=c["L"])
+        assert ids[0].tolist() == [i for i, _ in valid], c
+        assert dists[0].tolist() == [d for _, d in valid], c
+        assert (fl[0], E[0], S[0]) == (c["L"], c["E"], c["S"]), c
+    for c in boas:
+        q, r = queries[c["q"]]
+        for mode in MODES.values():
+            ids, dists, fl, E, S = gpu_search(gpu, q, r, k=c["k"], schedule=c["widths"], eps=c["eps"], **mode)
+            n = len(c["ids"])
+            assert ids[0, :n].tolist() == c["ids"] and (ids[0, n:] == PAD).all(), (c, mode)
+            assert dists[0, :n].tolist() == c["d"], (c, mode)
+            assert (fl[0], E[0], S[0]) == (c["final_L"], c["E"], c["S"]), (c, mode)
+    gpu.close()

@@ -16,8 +16,8 @@ from workloads import gen
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
-from helpers import (I32_MAX, I32_MIN, PAD, assert_same_up_to_near_ties, numpy_filtered_topk,
-                     numpy_valid, random_index, random_queries, ring_knn_graph)
+from helpers import (I32_MAX, I32_MIN, PAD, assert_same_up_to_near_ties, load_beam_trace,
+                     numpy_filtered_topk, numpy_valid, random_index, random_queries, ring_knn_graph)
 
 
 # ---------------------------------------------------------------------------
@@ -204,6 +204,44 @@ def test_empty_valid_set():
     res = oracle.boa(ix, q, r, 10, [16, 32])
     assert (res.ids == PAD).all() and np.isinf(res.dists).all()
     assert (res.final_L == 32).all()          # never confident: runs to the last width
+
+
+# ---------------------------------------------------------------------------
+# narrow widths, pinned by hand-traced searches (Sec. II "Beam search",
+# Alg. 2): which unexpanded entry goes next, merge-then-cut, exact seen-set
+# semantics, distance ties by id, padded rows, valid points reached only
+# through invalid ones, and the exact expansion and scored counts
+
+_TRACE = load_beam_trace(os.path.join(GOLDEN, "beam_trace.txt"))
+
+
+def _trace_index():
+    x, a, adj, entry, _, _, _ = _TRACE
+    return oracle.Index(x, a, np.zeros(1, np.int32), adj, entry)
+
+
+@pytest.mark.parametrize("case", _TRACE[5], ids=lambda c: f"{c['q']}-L{c['L']}")
+def test_search_matches_hand_trace(case):
+    ix = _trace_index()
+    q, r = _TRACE[4][case["q"]]
+    ids, ph, d, ln, E, S = oracle.search_lists(ix, q, r, case["L"])
+    n = len(case["ids"])
+    assert ln[0] == n
+    assert ids[0, :n].tolist() == case["ids"]
+    assert ph[0, :n].tolist() == case["phi"]
+    assert d[0, :n].tolist() == case["d"]
+    assert (E[0], S[0]) == (case["E"], case["S"])
+
+
+@pytest.mark.parametrize("case", _TRACE[6], ids=lambda c: f"{c['q']}-k{c['k']}-eps{c['eps']}")
+def test_boa_matches_hand_trace(case):
+    ix = _trace_index()
+    q, r = _TRACE[4][case["q"]]
+    res = oracle.boa(ix, q, r, case["k"], case["widths"], eps=case["eps"])
+    n = len(case["ids"])
+    assert res.ids[0, :n].tolist() == case["ids"] and (res.ids[0, n:] == PAD).all()
+    assert res.dists[0, :n].tolist() == case["d"]
+    assert (res.final_L[0], res.expansions[0], res.scored[0]) == (case["final_L"], case["E"], case["S"])
 
 
 # ---------------------------------------------------------------------------
