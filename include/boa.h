@@ -143,6 +143,33 @@ int boa_search(boa_index *idx, const void *queries, const int32_t *ranges, int64
                const boa_params *p, uint32_t *ids, float *dists, int32_t *final_L,
                uint32_t *expansions, uint32_t *scored, void *stream);
 
+/*
+ * Allocation-free variant of boa_search, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same arguments, results and error codes
+ * as boa_search; it calls no hipMalloc, hipFree or other allocating routine.
+ *   - Its work memory (active lists, counters, confidence flags, the visited
+ *     spill bitmaps) lives in one file-scope device array of
+ *     BOA_NOALLOC_SCRATCH_MB MiB per GPU, held by the library until the
+ *     process ends. Every call on a GPU shares that GPU's array: calls that
+ *     overlap on one GPU (other streams, other threads) race and must be
+ *     serialised by the caller. What must start at zero is cleared by a fill
+ *     kernel at the start of each call.
+ *   - nq <= BOA_NOALLOC_MAX_NQ, else BOA_EINVAL before any device work.
+ *   - BOA+ (boa_plus = 1) returns BOA_EUNSUPPORTED (it needs a second
+ *     stream). The other modes run; where the spill bitmaps of the planned
+ *     grid (n/8 bytes per resident wave) do not fit the array, the
+ *     persistent grid is made smaller (same results, less parallelism), and
+ *     an index whose single block does not fit returns BOA_EUNSUPPORTED.
+ *   - It keeps no statistics: boa_get_stats afterwards reports no search.
+ * It synchronises `stream` before returning, like boa_search.
+ */
+#define BOA_NOALLOC_SCRATCH_MB 64
+#define BOA_NOALLOC_MAX_NQ (1 << 18)
+int boa_search_noalloc(boa_index *idx, const void *queries, const int32_t *ranges, int64_t nq,
+                       const boa_params *p, uint32_t *ids, float *dists, int32_t *final_L,
+                       uint32_t *expansions, uint32_t *scored, void *stream);
+
 /* Statistics of the last boa_search on this index, one row per phase. */
 typedef struct {
     int32_t L;              /* phase beamwidth */

@@ -72,6 +72,8 @@ def lib():
                                                   P, C.c_int32, C.c_int64, C.POINTER(P)]
         L.boa_search.restype = C.c_int
         L.boa_search.argtypes = [P, P, P, C.c_int64, C.POINTER(Params), P, P, P, P, P, P]
+        L.boa_search_noalloc.restype = C.c_int
+        L.boa_search_noalloc.argtypes = [P, P, P, C.c_int64, C.POINTER(Params), P, P, P, P, P, P]
         L.boa_get_stats.restype = C.c_int
         L.boa_get_stats.argtypes = [P, C.POINTER(Stats)]
         L.boa_reset_counters.restype = C.c_int
@@ -147,7 +149,7 @@ class Index:
                eps: float = 0.05, tau: float = 0.0, fixed_L: int = 0, boa_plus: bool = False,
                sub_batches: int = 10, lds_hash_slots: int = 0, schedule=None, fused: bool = False,
                split: bool = False, counters: bool = False,
-               stream=None, out=None) -> SearchResult:
+               stream=None, out=None, no_alloc: bool = False) -> SearchResult:
         """Adaptive filtered top-k of a batch of device-resident queries.
 
         queries: torch tensor (nq, d) on the GPU, float32 or uint8 like the index.
@@ -187,7 +189,8 @@ class Index:
             p.schedule = C.cast(sched_arr, C.POINTER(C.c_int32))
             p.n_schedule = len(schedule)
         st = (stream if stream is not None else torch.cuda.current_stream(dev)).cuda_stream
-        _check(lib().boa_search(self._h, queries.data_ptr(), ranges.data_ptr(), nq, C.byref(p),
+        fn = lib().boa_search_noalloc if no_alloc else lib().boa_search
+        _check(fn(self._h, queries.data_ptr(), ranges.data_ptr(), nq, C.byref(p),
                                 ids.data_ptr(), dists.data_ptr(), fl.data_ptr(),
                                 E.data_ptr() if E is not None else None,
                                 S.data_ptr() if S is not None else None, st))

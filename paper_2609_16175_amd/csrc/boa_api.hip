@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -17,13 +18,17 @@ using namespace boa;
 
 namespace {
 
-thread_local std::string g_err;
+// last error message: a fixed per-thread buffer, so that reporting an error
+// allocates nothing
+thread_local char g_err[512];
 
-int fail(int code, const std::string &msg)
+int fail(int code, const char *msg)
 {
-    g_err = msg;
+    std::snprintf(g_err, sizeof(g_err), "%s", msg);
     return code;
 }
+
+int fail(int code, const std::string &msg) { return fail(code, msg.c_str()); }
 
 #define HIP_TRY(expr)                                                                  \
     do {                                                                               \
@@ -78,6 +83,13 @@ struct PhasePlan {
 
 }  // namespace
 
+// Scratch of the allocation-free search (boa_search_noalloc): one array per
+// GPU the library runs on, held until the process ends. Host code never
+// names it directly (in host code the name is a stand-in, not a device
+// address); it uses the address hipGetSymbolAddress returns for the current
+// device.
+static __device__ __align__(256) unsigned char scratch[(size_t)BOA_NOALLOC_SCRATCH_MB << 20];
+
 struct boa_index {
     int device = 0;
     int num_cu = 0;
@@ -123,7 +135,7 @@ struct boa_index {
 
 extern "C" {
 
-const char *boa_last_error(void) { return g_err.c_str(); }
+const char *boa_last_error(void) { return g_err; }
 
 void boa_default_params(boa_params *p)
 {
@@ -346,28 +358,29 @@ int ensure_workspace(boa_index *ix, int64_t nq, int32_t n_phases, uint64_t slots
 }
 
 // Beam schedule: L_{p+1} = min(ceil(alpha * L_p), Lmax); the phase at Lmax is the last.
-int make_schedule(const boa_params *p, std::vector<int32_t> &s)
+// (fixed-size output: the search path allocates no host memory either)
+int make_schedule(const boa_params *p, int32_t *s, int32_t *n)
 {
-    s.clear();
+    *n = 0;
     if (p->fixed_L > 0) {
-        s.push_back(p->fixed_L);
+        s[(*n)++] = p->fixed_L;
         return BOA_OK;
     }
     if (p->schedule && p->n_schedule > 0) {
+        if (p->n_schedule > BOA_MAX_PHASES) return fail(BOA_EINVAL, "too many phases");
         for (int i = 0; i < p->n_schedule; ++i) {
             if (p->schedule[i] < 1 || (i && p->schedule[i] <= p->schedule[i - 1]))
                 return fail(BOA_EINVAL, "schedule must be positive and strictly increasing");
-            s.push_back(p->schedule[i]);
+            s[(*n)++] = p->schedule[i];
         }
-        if ((int)s.size() > BOA_MAX_PHASES) return fail(BOA_EINVAL, "too many phases");
         return BOA_OK;
     }
     if (!(p->alpha > 1.0) || !std::isfinite(p->alpha)) return fail(BOA_EINVAL, "alpha must be > 1");
     if (p->L0 < 1 || p->Lmax < p->L0) return fail(BOA_EINVAL, "need 1 <= L0 <= Lmax");
     int64_t L = p->L0;
     for (;;) {
-        if ((int)s.size() >= BOA_MAX_PHASES) return fail(BOA_EINVAL, "schedule exceeds BOA_MAX_PHASES");
-        s.push_back((int32_t)L);
+        if (*n >= BOA_MAX_PHASES) return fail(BOA_EINVAL, "schedule exceeds BOA_MAX_PHASES");
+        s[(*n)++] = (int32_t)L;
         if (L >= p->Lmax) break;
         int64_t nx = (int64_t)std::ceil(p->alpha * (double)L);
         if (nx <= L) nx = L + 1;
@@ -514,22 +527,46 @@ PhasePlan plan_escalation(const boa_index *ix, int32_t L, int64_t S, int32_t for
     return dflt;
 }
 
-}  // namespace
+// Device memory one search works in: the index's grown-on-demand workspace
+// (boa_search) or a carve-out of the file-scope scratch array
+// (boa_search_noalloc).
+struct Workspace {
+    uint32_t *active[2];
+    uint32_t *n_active;       // 2 (BOA_MAX_PHASES + 1): per-phase active counts, BOA+ pool counts
+    uint32_t *counters;       // per-launch work counters
+    uint8_t *conf;            // nq
+    uint8_t *qstat;           // per phase x nq, with qE and qS (null: no per-phase statistics)
+    uint32_t *qE, *qS;
+    uint32_t *status;
+    uint32_t *bits;           // visited spill bitmaps, bits_words u32 per wave slot
+    uint32_t bits_words;
+    uint64_t slots;           // wave slots that have a spill bitmap
+    uint32_t *pool;           // BOA+ survivor pools, 2 nq (null: no BOA+)
+    bool timing;              // HIP events around launches; statistics of the search kept
+};
 
-extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_t nq,
-                          const boa_params *p, uint32_t *ids, float *dists, int32_t *final_L,
-                          uint32_t *expansions, uint32_t *scored, void *stream_v)
+// A validated search request (everything decided before device work).
+struct Request {
+    int32_t sched[BOA_MAX_PHASES];
+    int32_t n_phases;
+    bool plus, split, fused;
+    int32_t sub;              // BOA+ sub-batches (1 otherwise)
+    int32_t n_counters;
+    uint32_t tau_count;
+};
+
+int validate(const boa_index *ix, const void *queries, const int32_t *ranges, int64_t nq, const boa_params *p,
+             uint32_t *ids, float *dists, int32_t *final_L, Request &rq)
 {
     if (!ix || !p) return fail(BOA_EINVAL, "NULL index or params");
     if (nq < 0 || nq >= (int64_t)1 << 31) return fail(BOA_EINVAL, "nq out of range");
     if (nq > 0 && (!queries || !ranges || !ids || !dists || !final_L))
         return fail(BOA_EINVAL, "NULL device buffer");
-    std::vector<int32_t> sched;
-    int rc = make_schedule(p, sched);
+    int rc = make_schedule(p, rq.sched, &rq.n_phases);
     if (rc) return rc;
-    for (int32_t L : sched)
-        if (L < 1 || L > BOA_MAX_L) return fail(BOA_EINVAL, "beamwidth out of range [1, 2048]");
-    if (p->k < 1 || p->k > sched[0]) return fail(BOA_EINVAL, "need 1 <= k <= first-phase beamwidth");
+    for (int i = 0; i < rq.n_phases; ++i)
+        if (rq.sched[i] < 1 || rq.sched[i] > BOA_MAX_L) return fail(BOA_EINVAL, "beamwidth out of range [1, 2048]");
+    if (p->k < 1 || p->k > rq.sched[0]) return fail(BOA_EINVAL, "need 1 <= k <= first-phase beamwidth");
     if (!(p->eps >= 0.0) || !std::isfinite(p->eps)) return fail(BOA_EINVAL, "eps must be >= 0");
     if (!(p->tau >= 0.0 && p->tau < 1.0)) return fail(BOA_EINVAL, "tau must be in [0, 1)");
     if (p->lds_hash_slots && (p->lds_hash_slots < 64 || (p->lds_hash_slots & (p->lds_hash_slots - 1)) ||
@@ -537,67 +574,91 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
         return fail(BOA_EINVAL, "lds_hash_slots must be 0 or a power of two in [64, 16384]");
     if (p->lds_hash_slots && (uint32_t)p->lds_hash_slots < min_table_slots(ix))
         return fail(BOA_EINVAL, "lds_hash_slots too small for this index's id width");
-    const bool plus = p->boa_plus != 0 && p->fixed_L <= 0;
+    rq.plus = p->boa_plus != 0 && p->fixed_L <= 0;
     if (p->fused < 0 || p->fused > 2) return fail(BOA_EINVAL, "fused must be 0, 1 or 2");
-    const bool split = p->fused == 2;
-    const bool fused = p->fused == 1;
+    rq.split = p->fused == 2;
+    rq.fused = p->fused == 1;
     if (p->fused != 0 && p->tau != 0.0)
         return fail(BOA_EINVAL, "fused phases need tau == 0 (the residual test counts all queries of a phase)");
-    if (p->fused != 0 && plus) return fail(BOA_EINVAL, "fused and boa_plus are exclusive");
-    if (plus && p->tau != 0.0)
+    if (p->fused != 0 && rq.plus) return fail(BOA_EINVAL, "fused and boa_plus are exclusive");
+    if (rq.plus && p->tau != 0.0)
         return fail(BOA_EINVAL, "BOA+ needs tau == 0 (the residual test counts all queries of a phase)");
-    if (plus && (p->sub_batches < 1 || p->sub_batches > 1024)) return fail(BOA_EINVAL, "sub_batches out of range");
-    if (nq == 0) return BOA_OK;
+    if (rq.plus && (p->sub_batches < 1 || p->sub_batches > 1024)) return fail(BOA_EINVAL, "sub_batches out of range");
+    rq.sub = rq.plus ? std::min<int64_t>(p->sub_batches, std::max<int64_t>(nq, 1)) : 1;
+    rq.n_counters = rq.n_phases * (rq.sub + 1) + 8;
+    rq.tau_count = (uint32_t)std::floor(p->tau * (double)nq);
+    return BOA_OK;
+}
 
-    hipStream_t st = reinterpret_cast<hipStream_t>(stream_v);
-    int cur_dev = 0;
-    HIP_TRY(hipGetDevice(&cur_dev));
-    if (cur_dev != ix->device) return fail(BOA_EINVAL, "index lives on another device than the current one");
-
-    const int32_t n_phases = (int32_t)sched.size();
-    std::vector<PhasePlan> plans;
+// Launch plans of every phase, and the number of wave slots (spill bitmaps)
+// the search may use at once.
+int plan_search(const boa_index *ix, const Request &rq, int64_t nq, int32_t forced_h, PhasePlan *plans,
+                uint64_t *slots_out)
+{
     uint64_t slots = 0;
-    for (int32_t ph = 0; ph < n_phases; ++ph) {
+    const int32_t Lw = rq.sched[rq.n_phases - 1];
+    for (int32_t ph = 0; ph < rq.n_phases; ++ph) {
         // a fused launch, and a BOA+ escalation launch, size LDS for the widest phase
-        const bool wide = fused || (plus && ph > 0);
-        PhasePlan pl = plan_phase_widest(ix, wide ? sched.back() : sched[ph], p->lds_hash_slots, nq);
-        pl.L = sched[ph];
+        const bool wide = rq.fused || (rq.plus && ph > 0);
+        PhasePlan pl = plan_phase_widest(ix, wide ? Lw : rq.sched[ph], forced_h, nq);
+        pl.L = rq.sched[ph];
         if ((size_t)pl.lds_per_wave > ix->lds_per_block_max)
             return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
         slots = std::max<uint64_t>(slots, (uint64_t)pl.blocks * pl.wpb);
-        plans.push_back(pl);
+        plans[ph] = pl;
     }
-    if (split && n_phases > 1) {
+    if (rq.split && rq.n_phases > 1) {
         // every grid the escalation launch may take (it has at most nq waves)
-        const PhasePlan d = plan_phase(ix, sched.back(), p->lds_hash_slots, nq, true);
+        const PhasePlan d = plan_phase(ix, Lw, forced_h, nq, true);
         slots = std::max<uint64_t>(slots, (uint64_t)d.blocks * d.wpb);
-        if (p->lds_hash_slots <= 0)
+        if (forced_h <= 0)
             for (uint32_t h = 16384; h > (uint32_t)d.h_slots; h >>= 1) {
-                const PhasePlan c = plan_phase(ix, sched.back(), (int32_t)h, nq, true);
+                const PhasePlan c = plan_phase(ix, Lw, (int32_t)h, nq, true);
                 slots = std::max<uint64_t>(slots, (uint64_t)c.blocks * c.wpb);
             }
     }
-    const int32_t sub = plus ? std::min<int32_t>(p->sub_batches, (int32_t)nq) : 1;
-    const int32_t n_counters = n_phases * (sub + 1) + 8;
-    if ((rc = ensure_workspace(ix, nq, n_phases, plus ? 2 * slots : slots, n_counters, plus))) return rc;
-    if ((rc = ensure_events(ix, (size_t)n_phases * (sub + 1)))) return rc;
-    const uint32_t tau_count = (uint32_t)std::floor(p->tau * (double)nq);
+    *slots_out = slots;
+    return BOA_OK;
+}
+
+// Fewer blocks of a persistent launch (each wave pulls queries from the
+// launch's counter, so results do not change) where the workspace has spill
+// bitmaps for fewer wave slots than the plan would use.
+int cap_to_slots(PhasePlan &pl, uint64_t slots)
+{
+    const uint64_t b = slots / (uint64_t)pl.wpb;
+    if (b < 1) return fail(BOA_EUNSUPPORTED, "the index is too large for the scratch memory of this search");
+    if ((uint64_t)pl.blocks > b) pl.blocks = (int32_t)b;
+    return BOA_OK;
+}
+
+int run_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_t nq, const boa_params *p,
+               const Request &rq, PhasePlan *plans, uint32_t *ids, float *dists, int32_t *final_L,
+               uint32_t *expansions, uint32_t *scored, const Workspace &ws, hipStream_t st)
+{
+    const int32_t n_phases = rq.n_phases;
+    const int32_t *sched = rq.sched;
+    const int32_t Lw = sched[n_phases - 1];
+    for (int32_t ph = 0; ph < n_phases; ++ph)
+        if (int rc = cap_to_slots(plans[ph], ws.slots)) return rc;
 
     InitArgs ia{};
-    ia.active0 = ix->active[0];
-    ia.n_active = ix->n_active;
-    ia.counters = ix->counters;
-    ia.qstat = ix->qstat;
+    ia.active0 = ws.active[0];
+    ia.n_active = ws.n_active;
+    ia.counters = ws.counters;
+    ia.qstat = ws.qstat;
     ia.user_E = expansions;
     ia.user_S = scored;
-    ia.status = ix->status;
+    ia.status = ws.status;
     ia.nq = nq;
     ia.n_phases = n_phases;
-    ia.n_counters = n_counters;
+    ia.n_counters = rq.n_counters;
 
-    ix->launch_phase.clear();
+    if (ws.timing) {
+        ix->launch_phase.clear();
+        HIP_TRY(hipEventRecord(ix->ev_all0, st));
+    }
     ix->have_stats = false;
-    HIP_TRY(hipEventRecord(ix->ev_all0, st));
     HIP_TRY(launch_init(ia, st));
 
     PhaseArgs base{};
@@ -609,51 +670,58 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     base.final_L = final_L;
     base.user_E = expansions;
     base.user_S = scored;
-    base.bits = ix->bits;
-    base.bits_words = ix->bits_words;
+    base.bits = ws.bits;
+    base.bits_words = ws.bits_words;
     base.id_bits = id_bits(ix);
-    base.status = ix->status;
+    base.status = ws.status;
     base.eps = p->eps;
-    base.tau_count = tau_count;
+    base.tau_count = rq.tau_count;
     base.k = p->k;
-    base.conf = ix->conf;
+    base.conf = ws.conf;
     base.nq = nq;
-    base.qstat = ix->qstat;
-    base.qE = ix->qE;
-    base.qS = ix->qS;
+    base.qstat = ws.qstat;
+    base.qE = ws.qE;
+    base.qS = ws.qS;
     for (int32_t ph = 0; ph < n_phases; ++ph) base.sched[ph] = sched[ph];
     int ev = 0;
+    // one search launch, bracketed by HIP events when timing
+    auto launch = [&](const PhaseArgs &a, int blocks, hipStream_t s, bool wide, int phase) -> int {
+        if (ws.timing) HIP_TRY(hipEventRecord(ix->ev_start[ev], s));
+        HIP_TRY(launch_phase(a, ix->vec_dtype, blocks, s, wide));
+        if (ws.timing) {
+            HIP_TRY(hipEventRecord(ix->ev_end[ev], s));
+            ix->launch_phase.push_back({phase, ev});
+            ++ev;
+        }
+        return BOA_OK;
+    };
 
-    if (fused) {
+    if (rq.fused) {
         PhasePlan &pl = plans[0];
         PhaseArgs a = base;
-        a.active = ix->active[0];
-        a.n_active = ix->n_active;
+        a.active = ws.active[0];
+        a.n_active = ws.n_active;
         a.t_begin = 0;
         a.t_end = 0xFFFFFFFFu;
-        a.queue = ix->counters;
+        a.queue = ws.counters;
         a.p_begin = 0;
         a.p_end = n_phases;
-        a.L_alloc = sched.back();
+        a.L_alloc = Lw;
         a.h_log2 = ilog2((uint32_t)pl.h_slots);
         a.lds_per_wave = pl.lds_per_wave;
         a.waves_per_block = pl.wpb;
         a.slot_base = 0;
-        HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
-        HIP_TRY(launch_phase(a, ix->vec_dtype, pl.blocks, st));
-        HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
-        ix->launch_phase.push_back({0, ev});
-        ++ev;
+        if (int rc = launch(a, pl.blocks, st, false, 0)) return rc;
         pl.launches = 1;
-    } else if (split) {
+    } else if (rq.split) {
         // the first phase over every query at its own width ...
         PhasePlan &p0 = plans[0];
         PhaseArgs a = base;
-        a.active = ix->active[0];
-        a.n_active = ix->n_active;
+        a.active = ws.active[0];
+        a.n_active = ws.n_active;
         a.t_begin = 0;
         a.t_end = 0xFFFFFFFFu;
-        a.queue = ix->counters;
+        a.queue = ws.counters;
         a.p_begin = 0;
         a.p_end = 1;
         a.write_conf = 1;
@@ -662,40 +730,35 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
         a.lds_per_wave = p0.lds_per_wave;
         a.waves_per_block = p0.wpb;
         a.slot_base = 0;
-        HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
-        HIP_TRY(launch_phase(a, ix->vec_dtype, p0.blocks, st));
-        HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
-        ix->launch_phase.push_back({0, ev});
-        ++ev;
+        if (int rc = launch(a, p0.blocks, st, false, 0)) return rc;
         p0.launches = 1;
         if (n_phases > 1) {
             // ... then its survivors, compacted, through every later width
             CompactArgs ca{};
-            ca.in = ix->active[0];
-            ca.n_in = ix->n_active;
-            ca.conf = ix->conf;
-            ca.out = ix->active[1];
-            ca.n_out = ix->n_active + 1;
-            ca.tau_count = tau_count;
+            ca.in = ws.active[0];
+            ca.n_in = ws.n_active;
+            ca.conf = ws.conf;
+            ca.out = ws.active[1];
+            ca.n_out = ws.n_active + 1;
+            ca.tau_count = rq.tau_count;
             HIP_TRY(launch_compact(ca, st));
             uint32_t S = 0;
-            HIP_TRY(hipMemcpyAsync(&S, ix->n_active + 1, sizeof(S), hipMemcpyDeviceToHost, st));
+            HIP_TRY(hipMemcpyAsync(&S, ws.n_active + 1, sizeof(S), hipMemcpyDeviceToHost, st));
             HIP_TRY(hipStreamSynchronize(st));
             if (S > 0) {
-                PhasePlan pe = plan_escalation(ix, sched.back(), S, p->lds_hash_slots);
+                PhasePlan pe = plan_escalation(ix, Lw, S, p->lds_hash_slots);
                 if ((size_t)pe.lds_per_wave > (pe.vis_bitmap ? ix->lds_per_block_hw : ix->lds_per_block_max))
                     return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
-                if ((uint64_t)pe.blocks * pe.wpb > slots)
-                    return fail(BOA_EINVAL, "internal: escalation grid exceeds the spill bitmaps");
+                if (int rc = cap_to_slots(pe, ws.slots)) return rc;
                 PhaseArgs e = base;
-                e.active = ix->active[1];
-                e.n_active = ix->n_active + 1;
+                e.active = ws.active[1];
+                e.n_active = ws.n_active + 1;
                 e.t_begin = 0;
                 e.t_end = 0xFFFFFFFFu;
-                e.queue = ix->counters + 1;
+                e.queue = ws.counters + 1;
                 e.p_begin = 1;
                 e.p_end = n_phases;
-                e.L_alloc = sched.back();
+                e.L_alloc = Lw;
                 e.h_log2 = pe.vis_bitmap ? 3 : ilog2((uint32_t)pe.h_slots);   // (unused with the bitmap)
                 e.vis_bitmap = pe.vis_bitmap;
                 e.vis_words = pe.vis_bitmap ? (uint32_t)(((ix->view.n + 31) / 32 + 3) & ~(int64_t)3) : 0u;
@@ -708,31 +771,27 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
                 if (int rc2 = stage_profile_begin(&prof, pn, st)) return rc2;
                 e.prof = prof;
 #endif
-                HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
-                HIP_TRY(launch_phase(e, ix->vec_dtype, pe.blocks, st, true));
-                HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
+                if (int rc = launch(e, pe.blocks, st, true, 1)) return rc;
 #ifdef BOA_STAGE_PROFILE
                 std::fprintf(stderr, "[stage-profile] split escalation: %u survivors, table %d slots, %d waves\n",
                              S, pe.h_slots, pe.blocks * pe.wpb);
-                if (int rc2 = stage_profile_end(prof, pn, sched.back(), pe.blocks * pe.wpb, st)) return rc2;
+                if (int rc2 = stage_profile_end(prof, pn, Lw, pe.blocks * pe.wpb, st)) return rc2;
 #endif
-                ix->launch_phase.push_back({1, ev});
-                ++ev;
                 plans[1].launches = 1;
                 plans[1].h_slots = pe.h_slots;
                 plans[1].wpb = pe.wpb;
                 plans[1].blocks = pe.blocks;
             }
         }
-    } else if (!plus) {
+    } else if (!rq.plus) {
         for (int32_t ph = 0; ph < n_phases; ++ph) {
             PhasePlan &pl = plans[ph];
             PhaseArgs a = base;
-            a.active = ix->active[ph & 1];
-            a.n_active = ix->n_active + ph;
+            a.active = ws.active[ph & 1];
+            a.n_active = ws.n_active + ph;
             a.t_begin = 0;
             a.t_end = 0xFFFFFFFFu;
-            a.queue = ix->counters + ph;
+            a.queue = ws.counters + ph;
             a.p_begin = ph;
             a.p_end = ph + 1;
             a.write_conf = 1;
@@ -747,23 +806,19 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
             if (int rc2 = stage_profile_begin(&prof, pn, st)) return rc2;
             a.prof = prof;
 #endif
-            HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
-            HIP_TRY(launch_phase(a, ix->vec_dtype, pl.blocks, st));
-            HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
+            if (int rc = launch(a, pl.blocks, st, false, ph)) return rc;
 #ifdef BOA_STAGE_PROFILE
             if (int rc2 = stage_profile_end(prof, pn, pl.L, pl.blocks * pl.wpb, st)) return rc2;
 #endif
-            ix->launch_phase.push_back({ph, ev});
-            ++ev;
             pl.launches = 1;
             if (ph + 1 < n_phases) {
                 CompactArgs ca{};
-                ca.in = ix->active[ph & 1];
-                ca.n_in = ix->n_active + ph;
-                ca.conf = ix->conf;
-                ca.out = ix->active[(ph + 1) & 1];
-                ca.n_out = ix->n_active + ph + 1;
-                ca.tau_count = tau_count;
+                ca.in = ws.active[ph & 1];
+                ca.n_in = ws.n_active + ph;
+                ca.conf = ws.conf;
+                ca.out = ws.active[(ph + 1) & 1];
+                ca.n_out = ws.n_active + ph + 1;
+                ca.tau_count = rq.tau_count;
                 HIP_TRY(launch_compact(ca, st));
             }
         }
@@ -775,19 +830,25 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
         // runs; the second half's pooled survivors follow on the caller's
         // stream. Each escalation launch carries its queries through all
         // remaining widths (results are those of BOA).
+        if (!ws.pool || !ix->aux) return fail(BOA_EUNSUPPORTED, "BOA+ needs the index's own workspace");
+        const int32_t sub = rq.sub;
         const int64_t B = (nq + sub - 1) / sub;
         const int32_t nsub = (int32_t)((nq + B - 1) / B);
         const int32_t half = (nsub + 1) / 2;
-        uint32_t *pool[2] = {ix->pool, ix->pool + nq};
-        uint32_t *pool_n[2] = {ix->n_active + BOA_MAX_PHASES + 1, ix->n_active + BOA_MAX_PHASES + 2};
+        uint32_t *pool[2] = {ws.pool, ws.pool + nq};
+        uint32_t *pool_n[2] = {ws.n_active + BOA_MAX_PHASES + 1, ws.n_active + BOA_MAX_PHASES + 2};
+        // the second stream's waves use the spill bitmaps above the first's
+        const uint64_t half_slots = ws.slots / 2;
+        for (int32_t ph = 0; ph < n_phases; ++ph)
+            if (int rc = cap_to_slots(plans[ph], half_slots)) return rc;
         PhasePlan &p0 = plans[0];
         for (int32_t b = 0; b < nsub; ++b) {
             PhaseArgs a = base;
-            a.active = ix->active[0];
-            a.n_active = ix->n_active;
+            a.active = ws.active[0];
+            a.n_active = ws.n_active;
             a.t_begin = (uint32_t)(b * B);
             a.t_end = (uint32_t)std::min<int64_t>(nq, (b + 1) * B);
-            a.queue = ix->counters + b;
+            a.queue = ws.counters + b;
             a.p_begin = 0;
             a.p_end = 1;
             a.write_conf = 1;
@@ -798,15 +859,11 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
             a.slot_base = 0;
             const int64_t span = a.t_end - a.t_begin;
             const int blocks = (int)std::min<int64_t>(p0.blocks, (span + p0.wpb - 1) / p0.wpb);
-            HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
-            HIP_TRY(launch_phase(a, ix->vec_dtype, blocks, st));
-            HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
-            ix->launch_phase.push_back({0, ev});
-            ++ev;
+            if (int rc = launch(a, blocks, st, false, 0)) return rc;
             p0.launches += 1;
             AppendArgs ap{};
-            ap.in = ix->active[0] + a.t_begin;
-            ap.conf = ix->conf + a.t_begin;
+            ap.in = ws.active[0] + a.t_begin;
+            ap.conf = ws.conf + a.t_begin;
             ap.n = (uint32_t)span;
             const int g = b < half ? 0 : 1;
             ap.pool = pool[g];
@@ -822,19 +879,15 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
                 e.n_active = pool_n[0];
                 e.t_begin = 0;
                 e.t_end = 0xFFFFFFFFu;
-                e.queue = ix->counters + nsub;
+                e.queue = ws.counters + nsub;
                 e.p_begin = 1;
                 e.p_end = n_phases;
-                e.L_alloc = sched.back();
+                e.L_alloc = Lw;
                 e.h_log2 = ilog2((uint32_t)pe.h_slots);
                 e.lds_per_wave = pe.lds_per_wave;
                 e.waves_per_block = pe.wpb;
-                e.slot_base = (uint32_t)slots;   // disjoint spill bitmaps from stream 0
-                HIP_TRY(hipEventRecord(ix->ev_start[ev], ix->aux));
-                HIP_TRY(launch_phase(e, ix->vec_dtype, pe.blocks, ix->aux));
-                HIP_TRY(hipEventRecord(ix->ev_end[ev], ix->aux));
-                ix->launch_phase.push_back({1, ev});
-                ++ev;
+                e.slot_base = (uint32_t)half_slots;   // disjoint spill bitmaps from stream 0
+                if (int rc = launch(e, pe.blocks, ix->aux, false, 1)) return rc;
                 pe.launches += 1;
             }
         }
@@ -845,19 +898,15 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
             e.n_active = pool_n[1];
             e.t_begin = 0;
             e.t_end = 0xFFFFFFFFu;
-            e.queue = ix->counters + nsub + 1;
+            e.queue = ws.counters + nsub + 1;
             e.p_begin = 1;
             e.p_end = n_phases;
-            e.L_alloc = sched.back();
+            e.L_alloc = Lw;
             e.h_log2 = ilog2((uint32_t)pe.h_slots);
             e.lds_per_wave = pe.lds_per_wave;
             e.waves_per_block = pe.wpb;
             e.slot_base = 0;
-            HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
-            HIP_TRY(launch_phase(e, ix->vec_dtype, pe.blocks, st));
-            HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
-            ix->launch_phase.push_back({1, ev});
-            ++ev;
+            if (int rc = launch(e, pe.blocks, st, false, 1)) return rc;
             pe.launches += 1;
         }
         if (n_phases > 1) {
@@ -866,26 +915,134 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
         }
     }
 
-    HIP_TRY(hipEventRecord(ix->ev_all1, st));
+    if (ws.timing) HIP_TRY(hipEventRecord(ix->ev_all1, st));
     uint32_t status = 0;
-    HIP_TRY(hipMemcpyAsync(&status, ix->status, sizeof(uint32_t), hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipMemcpyAsync(&status, ws.status, sizeof(uint32_t), hipMemcpyDeviceToHost, st));
     HIP_TRY(hipStreamSynchronize(st));
-    ix->plans = plans;
-    ix->last_nq = nq;
-    ix->last_k = p->k;
-    ix->have_stats = true;
-    ix->cum_searches += 1;
-    for (auto &lp : ix->launch_phase) {
-        float ms = 0.f;
-        HIP_TRY(hipEventElapsedTime(&ms, ix->ev_start[lp.second], ix->ev_end[lp.second]));
-        ix->cum_kernel_ms += ms;
-        ix->cum_launches += 1;
-        ix->cum_phase_kernel_ms[lp.first] += ms;
-        ix->cum_phase_launches[lp.first] += 1;
+    if (ws.timing) {
+        ix->plans.assign(plans, plans + n_phases);
+        ix->last_nq = nq;
+        ix->last_k = p->k;
+        ix->have_stats = true;
+        ix->cum_searches += 1;
+        for (auto &lp : ix->launch_phase) {
+            float ms = 0.f;
+            HIP_TRY(hipEventElapsedTime(&ms, ix->ev_start[lp.second], ix->ev_end[lp.second]));
+            ix->cum_kernel_ms += ms;
+            ix->cum_launches += 1;
+            ix->cum_phase_kernel_ms[lp.first] += ms;
+            ix->cum_phase_launches[lp.first] += 1;
+        }
     }
     if (status & BOA_STATUS_OVERFLOW)
         return fail(BOA_EOVERFLOW, "a visited table overflowed; results are not valid");
     return BOA_OK;
+}
+
+constexpr size_t kScratchBytes = (size_t)BOA_NOALLOC_SCRATCH_MB << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+unsigned char *g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_for_device(int dev, unsigned char **out)
+{
+    if (dev < 0 || dev >= kMaxDevices) return fail(BOA_EUNSUPPORTED, "device ordinal beyond the scratch table");
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr) {
+            (void)hipGetLastError();
+            return fail(BOA_EHIP, "hipGetSymbolAddress of the scratch array failed");
+        }
+        g_scratch_ptr[dev] = reinterpret_cast<unsigned char *>(ptr);
+    }
+    *out = g_scratch_ptr[dev];
+    return BOA_OK;
+}
+
+}  // namespace
+
+extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_t nq,
+                          const boa_params *p, uint32_t *ids, float *dists, int32_t *final_L,
+                          uint32_t *expansions, uint32_t *scored, void *stream_v)
+{
+    Request rq;
+    if (int rc = validate(ix, queries, ranges, nq, p, ids, dists, final_L, rq)) return rc;
+    if (nq == 0) return BOA_OK;
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream_v);
+    int cur_dev = 0;
+    HIP_TRY(hipGetDevice(&cur_dev));
+    if (cur_dev != ix->device) return fail(BOA_EINVAL, "index lives on another device than the current one");
+
+    PhasePlan plans[BOA_MAX_PHASES];
+    uint64_t slots = 0;
+    if (int rc = plan_search(ix, rq, nq, p->lds_hash_slots, plans, &slots)) return rc;
+    if (int rc = ensure_workspace(ix, nq, rq.n_phases, rq.plus ? 2 * slots : slots, rq.n_counters, rq.plus))
+        return rc;
+    if (int rc = ensure_events(ix, (size_t)rq.n_phases * (rq.sub + 1))) return rc;
+    Workspace ws{};
+    ws.active[0] = ix->active[0];
+    ws.active[1] = ix->active[1];
+    ws.n_active = ix->n_active;
+    ws.counters = ix->counters;
+    ws.conf = ix->conf;
+    ws.qstat = ix->qstat;
+    ws.qE = ix->qE;
+    ws.qS = ix->qS;
+    ws.status = ix->status;
+    ws.bits = ix->bits;
+    ws.bits_words = ix->bits_words;
+    ws.slots = ix->slots_cap;
+    ws.pool = ix->pool;
+    ws.timing = true;
+    return run_search(ix, queries, ranges, nq, p, rq, plans, ids, dists, final_L, expansions, scored, ws, st);
+}
+
+extern "C" int boa_search_noalloc(boa_index *ix, const void *queries, const int32_t *ranges, int64_t nq,
+                                  const boa_params *p, uint32_t *ids, float *dists, int32_t *final_L,
+                                  uint32_t *expansions, uint32_t *scored, void *stream_v)
+{
+    Request rq;
+    if (int rc = validate(ix, queries, ranges, nq, p, ids, dists, final_L, rq)) return rc;
+    if (nq > BOA_NOALLOC_MAX_NQ) return fail(BOA_EINVAL, "nq exceeds the allocation-free search's maximum");
+    if (rq.plus) return fail(BOA_EUNSUPPORTED, "BOA+ needs a second stream: not available without allocation");
+    if (nq == 0) return BOA_OK;
+    hipStream_t st = reinterpret_cast<hipStream_t>(stream_v);
+    int cur_dev = 0;
+    HIP_TRY(hipGetDevice(&cur_dev));
+    if (cur_dev != ix->device) return fail(BOA_EINVAL, "index lives on another device than the current one");
+    unsigned char *base = nullptr;
+    if (int rc = scratch_for_device(cur_dev, &base)) return rc;
+
+    PhasePlan plans[BOA_MAX_PHASES];
+    uint64_t slots = 0;
+    if (int rc = plan_search(ix, rq, nq, p->lds_hash_slots, plans, &slots)) return rc;
+
+    // carve the scratch: fixed-size pieces first (256-byte aligned), then
+    // the spill bitmaps of as many wave slots as the rest holds
+    size_t off = 0;
+    auto take = [&](size_t bytes) -> unsigned char * {
+        unsigned char *q = base + off;
+        off += (bytes + 255) & ~(size_t)255;
+        return q;
+    };
+    Workspace ws{};
+    ws.n_active = reinterpret_cast<uint32_t *>(take(4 * 2 * (BOA_MAX_PHASES + 1)));
+    ws.status = reinterpret_cast<uint32_t *>(take(4 * 16));
+    ws.counters = reinterpret_cast<uint32_t *>(take(4 * (size_t)rq.n_counters));
+    ws.active[0] = reinterpret_cast<uint32_t *>(take(4 * (size_t)nq));
+    ws.active[1] = reinterpret_cast<uint32_t *>(take(4 * (size_t)nq));
+    ws.conf = reinterpret_cast<uint8_t *>(take((size_t)nq));
+    ws.qstat = nullptr;
+    ws.qE = ws.qS = nullptr;
+    ws.pool = nullptr;
+    ws.timing = false;
+    ws.bits_words = (uint32_t)(((ix->view.n + 127) / 128) * 4);
+    ws.bits = reinterpret_cast<uint32_t *>(base + off);
+    ws.slots = off < kScratchBytes ? (kScratchBytes - off) / ((size_t)ws.bits_words * 4) : 0;
+    if (ws.slots > slots) ws.slots = slots;
+    return run_search(ix, queries, ranges, nq, p, rq, plans, ids, dists, final_L, expansions, scored, ws, st);
 }
 
 extern "C" int boa_get_stats(const boa_index *ix, boa_stats *out)

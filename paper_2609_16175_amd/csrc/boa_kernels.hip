@@ -763,9 +763,11 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         const bool last = conf != 0u || p + 1 == a.p_end;
         if (lane == 0) {
             const size_t ps = (size_t)p * a.nq + qi;
-            a.qstat[ps] = (uint8_t)(1u + conf + (spill ? 4u : 0u));
-            a.qE[ps] = E;
-            a.qS[ps] = S;
+            if (a.qstat) {   // per-phase statistics (absent in the allocation-free search)
+                a.qstat[ps] = (uint8_t)(1u + conf + (spill ? 4u : 0u));
+                a.qE[ps] = E;
+                a.qS[ps] = S;
+            }
             if (a.user_E) a.user_E[qi] += E;
             if (a.user_S) a.user_S[qi] += S;
             if (a.write_conf) a.conf[t] = (uint8_t)conf;
@@ -864,7 +866,7 @@ __global__ void init_kernel(InitArgs a)
         if (a.user_E) a.user_E[i] = 0;
         if (a.user_S) a.user_S[i] = 0;
     }
-    if (i < (size_t)a.nq * a.n_phases) a.qstat[i] = 0;
+    if (a.qstat && i < (size_t)a.nq * a.n_phases) a.qstat[i] = 0;
     if (i < (size_t)a.n_counters) a.counters[i] = 0;
     if (i == 0) {
         a.n_active[0] = (uint32_t)a.nq;
