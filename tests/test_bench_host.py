@@ -59,28 +59,55 @@ def test_selectivity_summary():
 
 
 def test_recall_strict_and_tie_tolerant():
+    """Recall verifies every returned id on its own: its predicates, its
+    distance recomputed from the vectors, and repeats."""
     import numpy as np
     PAD = 0xFFFFFFFF
     k = 3
+    # points on one axis, queries at the origin: squared distance = x^2
+    x = np.array([7, 1, 2, 3, 8, 1, 2, 10, 11, 3, 3, 12], dtype=np.float32)
+    X = np.zeros((12, 4), dtype=np.float32)
+    X[:, 0] = x
+    a = np.zeros((12, 1), dtype=np.int32)
+    a[[5, 6], 0] = 1
+    a[10, 0] = 5
+    Q = np.zeros((3, 4), dtype=np.float32)
+    ranges = np.array([[[0, 0]], [[1, 1]], [[100, 200]]], dtype=np.int32)
     gt_ids = np.array([[1, 2, 3], [5, 6, -1], [0, 0, 0]], dtype=np.int64)
-    gt_d = np.array([[1.0, 2.0, 3.0], [1.0, 4.0, np.inf], [np.inf, np.inf, np.inf]])
-    n_valid = np.array([10, 2, 0])
+    gt_d = np.array([[1.0, 4.0, 9.0], [1.0, 4.0, np.inf], [np.inf, np.inf, np.inf]])
+    n_valid = np.array([9, 2, 0])
+
+    def rec(ids, per_query=False):
+        ver = bench.verified_rows(ids, X, Q, a, ranges, (0,))
+        return bench.recall(ids, gt_ids, gt_d, n_valid, k, ver, per_query=per_query)
+
     # query 0: ids 1, 2 right, 9 wrong but tied with the 3rd exact distance
     # query 1: both valid points found, then padding
     # query 2: no valid point, nothing returned
     ids = np.array([[1, 2, 9], [6, 5, PAD], [PAD, PAD, PAD]], dtype=np.uint32)
-    dists = np.array([[1.0, 2.0, 3.0], [4.0, 1.0, np.inf], [np.inf, np.inf, np.inf]], dtype=np.float32)
-    strict, tie = bench.recall(ids, dists, gt_ids, gt_d, n_valid, k)
-    per_q = bench.recall(ids, dists, gt_ids, gt_d, n_valid, k, per_query=True)
+    strict, tie = rec(ids)
     assert abs(strict - (2 / 3 + 1 + 1) / 3) < 1e-12
-    np.testing.assert_allclose(per_q, [1.0, 1.0, 1.0])
+    np.testing.assert_allclose(rec(ids, True), [1.0, 1.0, 1.0])
     assert abs(tie - 1.0) < 1e-12
     # a farther wrong id is not forgiven
     ids2 = ids.copy()
-    dists2 = dists.copy()
-    dists2[0, 2] = 3.5
-    per_q2 = bench.recall(ids2, dists2, gt_ids, gt_d, n_valid, k, per_query=True)
-    assert abs(per_q2[0] - 2 / 3) < 1e-12
+    ids2[0, 2] = 4
+    assert abs(rec(ids2, True)[0] - 2 / 3) < 1e-12
+    # an id that violates its query's predicate counts for nothing, even at
+    # the tied distance
+    ids3 = ids.copy()
+    ids3[0, 2] = 10
+    assert abs(rec(ids3, True)[0] - 2 / 3) < 1e-12
+    # a repeated id counts once
+    ids4 = ids.copy()
+    ids4[0] = [1, 1, 2]
+    assert abs(rec(ids4, True)[0] - 2 / 3) < 1e-12
+    s4, _ = rec(ids4)
+    assert abs(s4 - (2 / 3 + 1 + 1) / 3) < 1e-12
+    # returning an id where no point is valid scores 0
+    ids5 = ids.copy()
+    ids5[2, 0] = 3
+    assert rec(ids5, True)[2] == 0.0
 
 
 def test_exact_filtered_topk_matches_brute_force():

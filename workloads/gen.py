@@ -245,8 +245,8 @@ def _quantile_window(g, nq: int, column_sorted: np.ndarray, frac: float) -> np.n
     return np.stack([column_sorted[i0], column_sorted[i1]], axis=1)
 
 
-def _ranges(wl: Workload, attrs: np.ndarray, nq: int, qcid: np.ndarray) -> np.ndarray:
-    g = _rng(wl.seed, 5)
+def _ranges(wl: Workload, attrs: np.ndarray, nq: int, qcid: np.ndarray, part: int = 5) -> np.ndarray:
+    g = _rng(wl.seed, part)
     r = np.empty((nq, wl.m, 2), dtype=np.int32)
     if wl.kind == "tiny":
         r[:, 0, :] = _uniform_window(g, nq, 1000, np.full(nq, 500))
@@ -289,3 +289,13 @@ def generate(wl: Workload) -> Data:
     queries, qcid = _mixture_rows(wl, centres, wl.nq, part=4)
     ranges = _ranges(wl, attrs, wl.nq, qcid)
     return Data(wl, vectors, attrs, queries, ranges, qcid)
+
+
+def heldout_queries(wl: Workload, data: Data, nq: int):
+    """A second query batch of the same recipe (other seed parts): queries,
+    ranges and generating clusters of `nq` fresh draws. Used to choose
+    search parameters without looking at the batch they are reported on."""
+    centres = _centres(wl)
+    queries, qcid = _mixture_rows(wl, centres, nq, part=7)
+    ranges = _ranges(wl, data.attrs, nq, qcid, part=8)
+    return queries, ranges, qcid
