@@ -64,6 +64,7 @@ enum { BOA_ATTR_I32 = 0, BOA_ATTR_F32 = 1 };
 #define BOA_MAX_L 2048       /* beamwidth */
 #define BOA_MAX_PHASES 32
 #define BOA_MAX_N ((int64_t)1 << 24) /* ids are packed into 24 bits */
+#define BOA_MAX_BUILD_N ((int64_t)2 << 20) /* graph construction inside the library */
 
 /*
  * Build an index from host arrays (copied into device memory; the caller
@@ -74,13 +75,24 @@ enum { BOA_ATTR_I32 = 0, BOA_ATTR_F32 = 1 };
  *   attr_dtypes host, m entries of BOA_ATTR_I32 / BOA_ATTR_F32.
  *   adjacency   host, row-major n x R uint32 neighbour ids, padded with
  *               0xFFFFFFFF; 1 <= R <= BOA_MAX_R. A row may not hold its own
- *               id, nor any id twice. (Graph construction is an offline step:
- *               Sec. II.)
- *   entry       the entry point s of every search (Alg. 2), 0 <= entry < n.
+ *               id, nor any id twice.
+ *               NULL: the library builds the graph (Sec. II "Graph
+ *               construction": DiskANN alpha-pruning, alpha = 1.2, of each
+ *               point's min(2R, 128) exact nearest neighbours, then of its
+ *               forward and reverse neighbours to R - 1 edges, then every
+ *               point made reachable from the entry point through an in-edge
+ *               from its nearest reachable candidate). Needs n <=
+ *               BOA_MAX_BUILD_N (the candidates come from a brute-force
+ *               scan), else BOA_EUNSUPPORTED.
+ *   R           the row width, 1 <= R <= BOA_MAX_R: one neighbour per lane of
+ *               a 64-wide wavefront.
+ *   entry       the entry point s of every search (Alg. 2), 0 <= entry < n;
+ *               -1: the medoid, the point nearest (float64) to the float64
+ *               centroid of the vectors, ties to the lowest id.
  *   n           1 <= n < BOA_MAX_N.
  *   out         receives the index; free it with boa_free_index.
  * Errors: BOA_EINVAL (bad sizes, null pointers, out-of-range ids in the
- * adjacency), BOA_ENOMEM, BOA_EHIP.
+ * adjacency), BOA_EUNSUPPORTED, BOA_ENOMEM, BOA_EHIP.
  */
 int boa_build_index_from_arrays(const void *vectors, int64_t n, int32_t d, int32_t vec_dtype,
                                 const int32_t *attrs, int32_t m, const int32_t *attr_dtypes,
@@ -205,6 +217,12 @@ int boa_get_stats(const boa_index *idx, boa_stats *out);
 
 /* Zero the accumulated counters of boa_stats. */
 int boa_reset_counters(boa_index *idx);
+
+/* The graph and entry point an index searches (e.g. the ones the library
+ * built). adjacency: HOST n x R uint32, or NULL; entry: the entry point s,
+ * or NULL; repaired: in-edges the library's construction added to reach
+ * every point (-1 when the caller passed the adjacency), or NULL. */
+int boa_get_graph(const boa_index *idx, uint32_t *adjacency, int64_t *entry, int64_t *repaired);
 
 void boa_free_index(boa_index *idx);
 

@@ -78,6 +78,8 @@ def lib():
         L.boa_get_stats.argtypes = [P, C.POINTER(Stats)]
         L.boa_reset_counters.restype = C.c_int
         L.boa_reset_counters.argtypes = [P]
+        L.boa_get_graph.restype = C.c_int
+        L.boa_get_graph.argtypes = [P, P, C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
         L.boa_free_index.restype = None
         L.boa_free_index.argtypes = [P]
         L.boa_last_error.restype = C.c_char_p
@@ -111,8 +113,11 @@ class SearchResult:
 class Index:
     """A graph index resident in device memory (owned by libboa)."""
 
-    def __init__(self, vectors: np.ndarray, attrs: np.ndarray, attr_dtypes, adjacency: np.ndarray,
-                 entry: int):
+    def __init__(self, vectors: np.ndarray, attrs: np.ndarray, attr_dtypes, adjacency, entry: int = -1,
+                 R: int = 0):
+        """adjacency: n x R uint32 rows, or None to have the library build the
+        graph with R edges per row; entry: the entry point, or -1 for the
+        medoid (computed by the library)."""
         vectors = np.ascontiguousarray(vectors)
         if vectors.dtype == np.float32:
             vt = VEC_F32
@@ -122,17 +127,32 @@ class Index:
             raise TypeError("vectors must be float32 or uint8")
         attrs = np.ascontiguousarray(attrs, dtype=np.int32)
         types = np.ascontiguousarray(attr_dtypes, dtype=np.int32)
-        adj = np.ascontiguousarray(adjacency, dtype=np.uint32)
         n, d = vectors.shape
-        if attrs.shape != (n, types.shape[0]) or adj.shape[0] != n:
-            raise ValueError("shape mismatch between vectors, attributes and adjacency")
+        if adjacency is None:
+            adj, width, aptr = None, int(R), None
+        else:
+            adj = np.ascontiguousarray(adjacency, dtype=np.uint32)
+            width, aptr = adj.shape[1], adj.ctypes.data
+            if adj.shape[0] != n:
+                raise ValueError("shape mismatch between vectors and adjacency")
+        if attrs.shape != (n, types.shape[0]):
+            raise ValueError("shape mismatch between vectors and attributes")
         h = C.c_void_p()
         _check(lib().boa_build_index_from_arrays(vectors.ctypes.data, n, d, vt, attrs.ctypes.data,
-                                                 types.shape[0], types.ctypes.data, adj.ctypes.data,
-                                                 adj.shape[1], int(entry), C.byref(h)))
+                                                 types.shape[0], types.ctypes.data, aptr,
+                                                 width, int(entry), C.byref(h)))
         self._h = h
-        self.n, self.d, self.m, self.R = n, d, types.shape[0], adj.shape[1]
+        self.n, self.d, self.m, self.R = n, d, types.shape[0], width
         self.vec_dtype = vt
+
+    def graph(self):
+        """(adjacency n x R uint32, entry, repaired): the graph the index
+        searches; repaired counts the in-edges the library's construction
+        added to reach every point (-1 when the caller gave the graph)."""
+        adj = np.empty((self.n, self.R), dtype=np.uint32)
+        e, rep = C.c_int64(), C.c_int64()
+        _check(lib().boa_get_graph(self._h, adj.ctypes.data, C.byref(e), C.byref(rep)))
+        return adj, int(e.value), int(rep.value)
 
     def close(self):
         if getattr(self, "_h", None):

@@ -6,7 +6,7 @@ import subprocess
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SOURCES = [os.path.join(PKG, "csrc", f) for f in ("boa_kernels.hip", "boa_api.hip")]
+SOURCES = [os.path.join(PKG, "csrc", f) for f in ("boa_kernels.hip", "boa_build.hip", "boa_api.hip")]
 LIB = os.path.join(PKG, "libboa.so")
 
 HIPCC_FLAGS = [

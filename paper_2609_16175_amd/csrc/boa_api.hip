@@ -101,6 +101,9 @@ struct boa_index {
     int32_t *d_attrs = nullptr;
     uint32_t *d_adj = nullptr;
 
+    bool built_graph = false;        // the graph was constructed by the library
+    BuildStats build_stats{};
+
     // workspace, grown on demand
     int64_t nq_cap = 0;
     int32_t ph_cap = 0;
@@ -194,22 +197,23 @@ int boa_build_index_from_arrays(const void *vectors, int64_t n, int32_t d, int32
     if (!out) return fail(BOA_EINVAL, "out is NULL");
     *out = nullptr;
     if (!vectors || !attrs || !attr_dtypes) return fail(BOA_EINVAL, "NULL input array");
-    if (!adjacency)
-        return fail(BOA_EUNSUPPORTED, "graph construction is not part of this library; pass an adjacency");
     if (n < 1 || n >= BOA_MAX_N) return fail(BOA_EINVAL, "n out of range [1, 2^24)");
+    if (!adjacency && n > BOA_MAX_BUILD_N)
+        return fail(BOA_EUNSUPPORTED, "graph construction by exact nearest neighbours is limited to "
+                                      "BOA_MAX_BUILD_N points; pass an adjacency");
     if (vec_dtype != BOA_VEC_F32 && vec_dtype != BOA_VEC_U8) return fail(BOA_EINVAL, "bad vec_dtype");
     if (d < 4 || d > 1024) return fail(BOA_EINVAL, "d out of range [4, 1024]");
     if (vec_dtype == BOA_VEC_F32 && d % 4) return fail(BOA_EINVAL, "float32 vectors need d % 4 == 0");
     if (vec_dtype == BOA_VEC_U8 && d % 16) return fail(BOA_EINVAL, "uint8 vectors need d % 16 == 0");
     if (m < 1 || m > BOA_MAX_M) return fail(BOA_EINVAL, "m out of range [1, 8]");
     if (R < 1 || R > BOA_MAX_R) return fail(BOA_EINVAL, "R out of range [1, 64]");
-    if (entry < 0 || entry >= n) return fail(BOA_EINVAL, "entry out of range");
+    if (entry < -1 || entry >= n) return fail(BOA_EINVAL, "entry out of range (-1: the medoid)");
     uint32_t f32_mask = 0;
     for (int j = 0; j < m; ++j) {
         if (attr_dtypes[j] == BOA_ATTR_F32) f32_mask |= 1u << j;
         else if (attr_dtypes[j] != BOA_ATTR_I32) return fail(BOA_EINVAL, "bad attribute dtype");
     }
-    {
+    if (adjacency) {
         std::vector<uint32_t> row((size_t)R);
         for (int64_t u = 0; u < n; ++u) {
             int cnt = 0;
@@ -265,9 +269,30 @@ int boa_build_index_from_arrays(const void *vectors, int64_t n, int32_t d, int32
     }
     if (hipMemcpy(ix->d_vectors, vectors, (size_t)n * d * esz, hipMemcpyHostToDevice) != hipSuccess ||
         hipMemcpy(ix->d_attrs, attr_src, (size_t)n * m_pad * 4, hipMemcpyHostToDevice) != hipSuccess ||
-        hipMemcpy(ix->d_adj, adjacency, (size_t)n * R * 4, hipMemcpyHostToDevice) != hipSuccess) {
+        (adjacency && hipMemcpy(ix->d_adj, adjacency, (size_t)n * R * 4, hipMemcpyHostToDevice) != hipSuccess)) {
         boa_free_index(ix);
         return fail(BOA_EHIP, "index upload failed");
+    }
+    // the entry point s of Alg. 2: the medoid unless the caller names one
+    if (entry < 0) {
+        uint32_t s = 0;
+        hipError_t e = compute_medoid(ix->d_vectors, n, d, vec_dtype, &s);
+        if (e != hipSuccess) {
+            boa_free_index(ix);
+            return fail(BOA_EHIP, std::string("medoid computation failed: ") + hipGetErrorString(e));
+        }
+        entry = s;
+    }
+    if (!adjacency) {
+        BuildStats bs{};
+        hipError_t e = build_graph(ix->d_vectors, n, d, vec_dtype, R, (uint32_t)entry, ix->d_adj, &bs);
+        if (e != hipSuccess) {
+            boa_free_index(ix);
+            return fail(e == hipErrorOutOfMemory ? BOA_ENOMEM : BOA_EHIP,
+                        std::string("graph construction failed: ") + hipGetErrorString(e));
+        }
+        ix->built_graph = true;
+        ix->build_stats = bs;
     }
     ix->view.vectors = ix->d_vectors;
     ix->view.attrs = ix->d_attrs;
@@ -1106,6 +1131,20 @@ extern "C" int boa_reset_counters(boa_index *ix)
     for (int i = 0; i < BOA_MAX_PHASES; ++i) {
         ix->cum_phase_launches[i] = 0;
         ix->cum_phase_kernel_ms[i] = 0.0;
+    }
+    return BOA_OK;
+}
+
+extern "C" int boa_get_graph(const boa_index *ix, uint32_t *adjacency, int64_t *entry, int64_t *repaired)
+{
+    if (!ix) return fail(BOA_EINVAL, "NULL index");
+    if (entry) *entry = ix->view.entry;
+    if (repaired) *repaired = ix->built_graph ? ix->build_stats.repaired : -1;
+    if (adjacency) {
+        int cur = 0;
+        HIP_TRY(hipGetDevice(&cur));
+        if (cur != ix->device) return fail(BOA_EINVAL, "index lives on another device than the current one");
+        HIP_TRY(hipMemcpy(adjacency, ix->d_adj, (size_t)ix->view.n * ix->view.R * 4, hipMemcpyDeviceToHost));
     }
     return BOA_OK;
 }

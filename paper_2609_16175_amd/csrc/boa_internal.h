@@ -88,6 +88,18 @@ struct InitArgs {
     int32_t n_counters;
 };
 
+// Index construction (boa_build.hip): the medoid entry point, and the graph
+// when the caller passes no adjacency.
+struct BuildStats {
+    int32_t K;                 // exact nearest candidates per point
+    int64_t edges;             // edges of the final graph
+    int64_t repaired;          // in-edges added to reach every point from s
+    int64_t repair_fallback;   // of which not from the point's own candidates
+};
+hipError_t compute_medoid(const void *d_vectors, int64_t n, int32_t d, int vec_dtype, uint32_t *entry);
+hipError_t build_graph(const void *d_vectors, int64_t n, int32_t d, int vec_dtype, int32_t R, uint32_t entry,
+                       uint32_t *d_adj, BuildStats *stats);
+
 // wide: the scorer variant with twice the rows in flight (for launches that
 // hold few waves per CU)
 hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st, bool wide = false);

@@ -77,9 +77,16 @@ def test_build_validation(over, needle):
     assert rc == -1 and needle in msg
 
 
-def test_build_without_adjacency_is_unsupported():
-    rc, msg = _build(adj=None)
-    assert rc == -4
+def test_build_without_adjacency_beyond_the_build_limit_is_unsupported():
+    # the library builds the graph itself only up to BOA_MAX_BUILD_N points;
+    # refused before any array is read or any device work
+    rc, msg = _build(adj=None, n=(2 << 20) + 1)
+    assert rc == -4 and "BOA_MAX_BUILD_N" in msg
+
+
+def test_entry_below_minus_one_is_invalid():
+    rc, msg = _build(entry=-2)
+    assert rc == -1 and "entry" in msg
 
 
 def test_search_null_index():
