@@ -62,6 +62,9 @@ def lib():
         L.orc_boa.restype = C.c_int32
         L.orc_boa.argtypes = [C.POINTER(_Index), P, P, C.c_int64, C.c_int32, P, C.c_int32,
                               C.c_double, C.c_double, P, P, P, P, P, P, C.c_int32]
+        L.orc_boa_warm.restype = C.c_int32
+        L.orc_boa_warm.argtypes = [C.POINTER(_Index), P, P, C.c_int64, C.c_int32, P, C.c_int32,
+                                   C.c_double, P, P, P, P, P, P]
         L.orc_search_lists.restype = C.c_int32
         L.orc_search_lists.argtypes = [C.POINTER(_Index), P, P, C.c_int64, C.c_int32,
                                        P, P, P, P, P, P]
@@ -168,6 +171,27 @@ def boa(ix: Index, queries, ranges, k: int, sched: list[int], eps: float = 0.05,
     st = np.zeros((len(s), 5), dtype=np.int64)
     n = lib().orc_boa(C.byref(ix._c), _p(q), _p(r), nq, k, _p(s), len(s), eps, tau,
                       _p(ids), _p(dists), _p(fl), _p(E), _p(S), _p(st), threads)
+    if n < 0:
+        raise MemoryError("oracle allocation failed")
+    phases = [dict(L=int(a[0]), active=int(a[1]), confident=int(a[2]), expansions=int(a[3]),
+                   scored=int(a[4])) for a in st[:n]]
+    return BoaResult(ids, dists, fl, E, S, phases)
+
+
+def boa_warm(ix: Index, queries, ranges, k: int, sched: list[int], eps: float = 0.05) -> BoaResult:
+    """Multi-phase search with warm-start escalation (each phase continues
+    from the previous phase's list and scored set; see orc_boa_warm)."""
+    q, r = ix._q(queries, ranges)
+    nq = q.shape[0]
+    s = np.ascontiguousarray(sched, dtype=np.int32)
+    ids = np.full((nq, k), PAD, dtype=np.uint32)
+    dists = np.full((nq, k), np.inf, dtype=np.float32)
+    fl = np.zeros(nq, dtype=np.int32)
+    E = np.zeros(nq, dtype=np.int64)
+    S = np.zeros(nq, dtype=np.int64)
+    st = np.zeros((len(s), 5), dtype=np.int64)
+    n = lib().orc_boa_warm(C.byref(ix._c), _p(q), _p(r), nq, k, _p(s), len(s), eps,
+                           _p(ids), _p(dists), _p(fl), _p(E), _p(S), _p(st))
     if n < 0:
         raise MemoryError("oracle allocation failed")
     phases = [dict(L=int(a[0]), active=int(a[1]), confident=int(a[2]), expansions=int(a[3]),

@@ -495,3 +495,124 @@ int32_t orc_bruteforce(const orc_index *ix, const void *queries, const int32_t *
     free(best);
     return 0;
 }
+
+/* ------------------------------------------------------------------------
+ * Warm-start escalation (Sec. III-A "Redundancy Avoidance": a query that
+ * runs at width L and then at alpha L should not redo the width-L work;
+ * the width-L phase keeps its best L results and the next phase adds the
+ * next alpha L - L). That paragraph is garbled; READING:
+ *   - during phase p (width L_p) the query's sorted candidate list holds up
+ *     to L_{p+1} entries (its own width at the last phase): new candidates
+ *     are merged into it and it is cut to that capacity, but only entries
+ *     among its first L_p are expanded (still one per iteration, the first
+ *     unexpanded one), and the phase ends when those are all expanded;
+ *   - the first L_p entries are the phase's worklist: the result and the
+ *     confidence test (Eq. 3) read them; they equal the worklist of a fresh
+ *     width-L_p search (the best L_p of a longer list of everything scored
+ *     are the best L_p of everything scored), so phase 0 is unchanged;
+ *   - a query that escalates keeps its list, expanded flags and set of
+ *     scored nodes: phase p+1 continues from them instead of restarting at
+ *     s. E and S count each phase's own new work.
+ * Queries are independent, so each runs its phases back to back here (the
+ * residual fraction tau is 0 in this mode). */
+static void search_continue(const orc_index *ix, orc_ws *w, const void *q, const int32_t *rr, int32_t L_sel,
+                            int32_t L_cap, int *len_io, int64_t *E, int64_t *S)
+{
+    orc_entry *beam = w->beam, *cand = w->cand, *tmp = w->tmp;
+    int len = *len_io;
+    for (;;) {
+        int lim = len < L_sel ? len : L_sel;
+        int j = 0;
+        while (j < lim && beam[j].expanded) ++j;
+        if (j == lim) break; /* the phase's worklist is fully expanded */
+        beam[j].expanded = 1;
+        uint32_t u = beam[j].id;
+        *E += 1;
+
+        int c = 0;
+        for (int r = 0; r < ix->R; ++r) {
+            uint32_t v = ix->adj[(int64_t)u * ix->R + r];
+            if (v == ORC_PAD) continue;
+            if (w->stamp[v] == w->cur) continue;
+            w->stamp[v] = w->cur;
+            cand[c++] = score(ix, v, q, rr);
+        }
+        *S += c;
+
+        for (int a = 1; a < c; ++a) {
+            orc_entry x = cand[a];
+            int b = a - 1;
+            while (b >= 0 && entry_before(&x, &cand[b])) { cand[b + 1] = cand[b]; --b; }
+            cand[b + 1] = x;
+        }
+        int ia = 0, ib = 0, o = 0;
+        while ((ia < len || ib < c) && o < L_cap) {
+            if (ib >= c || (ia < len && entry_before(&beam[ia], &cand[ib])))
+                tmp[o++] = beam[ia++];
+            else
+                tmp[o++] = cand[ib++];
+        }
+        memcpy(beam, tmp, sizeof(orc_entry) * (size_t)o);
+        len = o;
+    }
+    *len_io = len;
+}
+
+int32_t orc_boa_warm(const orc_index *ix, const void *queries, const int32_t *ranges, int64_t nq, int32_t k,
+                     const int32_t *schedule, int32_t n_phases, double eps, uint32_t *ids, float *dists,
+                     int32_t *final_L, int64_t *q_E, int64_t *q_S, int64_t *phase_stats)
+{
+    if (nq <= 0 || n_phases <= 0) return 0;
+    int32_t Lmax = 0;
+    for (int p = 0; p < n_phases; ++p) if (schedule[p] > Lmax) Lmax = schedule[p];
+    orc_ws w;
+    if (!ws_init(&w, ix, Lmax)) return -2;
+    float *vd = (float *)malloc(sizeof(float) * (size_t)Lmax);
+    if (!vd) { ws_free(&w); return -2; }
+    size_t qbytes = (size_t)ix->d * (ix->vec_dtype == ORC_VEC_U8 ? 1 : 4);
+    if (phase_stats) memset(phase_stats, 0, sizeof(int64_t) * 5 * (size_t)n_phases);
+    int32_t ran = 0;
+    for (int64_t i = 0; i < nq; ++i) {
+        const void *q = (const char *)queries + (size_t)i * qbytes;
+        const int32_t *rr = ranges + i * ix->m * 2;
+        int64_t Et = 0, St = 0;
+        /* the entry point, scored and marked before the first expansion */
+        ws_new_search(&w, ix->n);
+        int len = 1;
+        w.beam[0] = score(ix, (uint32_t)ix->entry, q, rr);
+        w.stamp[ix->entry] = w.cur;
+        int64_t S0 = 1;
+        for (int p = 0; p < n_phases; ++p) {
+            int32_t L = schedule[p];
+            int32_t cap = p + 1 < n_phases ? schedule[p + 1] : L;
+            int64_t E = 0, S = S0;
+            S0 = 0;
+            search_continue(ix, &w, q, rr, L, cap, &len, &E, &S);
+            int lim = len < L ? len : L;
+            int n_valid = 0;
+            while (n_valid < lim && w.beam[n_valid].phi == 0) { vd[n_valid] = w.beam[n_valid].d; ++n_valid; }
+            for (int a = 0; a < k; ++a) {
+                ids[i * k + a] = a < n_valid ? w.beam[a].id : ORC_PAD;
+                dists[i * k + a] = a < n_valid ? w.beam[a].d : INFINITY;
+            }
+            final_L[i] = L;
+            Et += E;
+            St += S;
+            int conf = orc_confident(vd, n_valid, k, eps);
+            if (phase_stats) {
+                phase_stats[p * 5 + 0] = L;
+                phase_stats[p * 5 + 1] += 1;
+                phase_stats[p * 5 + 2] += conf;
+                phase_stats[p * 5 + 3] += E;
+                phase_stats[p * 5 + 4] += S;
+            }
+            if (p + 1 > ran) ran = p + 1;
+            if (conf) break;
+        }
+        if (q_E) q_E[i] = Et;
+        if (q_S) q_S[i] = St;
+    }
+    free(vd);
+    ws_free(&w);
+    return ran;
+}

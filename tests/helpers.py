@@ -107,8 +107,9 @@ def assert_same_up_to_near_ties(ids, dists, ref_ids, ref_d64, rel=1e-5):
 def load_beam_trace(path):
     """The hand-traced golden graph of tests/golden/beam_trace.txt:
     (vectors n x 4 float32, attrs n x 1, adjacency n x 3, entry, queries
-    {name: (q, ranges)}, SEARCH cases, BOA cases)."""
+    {name: (q, ranges)}, SEARCH cases, BOA cases, WARM cases)."""
     pts, adj, queries, searches, boas, entry = {}, {}, {}, [], [], None
+    warms = []
     with open(path) as f:
         for line in f:
             p = line.split()
@@ -128,9 +129,9 @@ def load_beam_trace(path):
                 searches.append(dict(q=p[1], L=int(p[2]), E=int(p[3]), S=int(p[4]),
                                      ids=[a for a, _, _ in items], phi=[b for _, b, _ in items],
                                      d=[c for _, _, c in items]))
-            elif p[0] == "BOA":
+            elif p[0] in ("BOA", "WARM"):
                 items = [tuple(int(t) for t in s.split("/")) for s in p[8:]]
-                boas.append(dict(q=p[1], k=int(p[2]), eps=float(p[3]),
+                (boas if p[0] == "BOA" else warms).append(dict(q=p[1], k=int(p[2]), eps=float(p[3]),
                                  widths=[int(w) for w in p[4].split(",")], final_L=int(p[5]),
                                  E=int(p[6]), S=int(p[7]), ids=[a for a, _ in items],
                                  d=[b for _, b in items]))
@@ -141,4 +142,4 @@ def load_beam_trace(path):
         x[i, :2] = (px, py)
         a[i, 0] = av
     A = np.array([adj[i] for i in range(n)], dtype=np.uint32)
-    return x, a, A, entry, queries, searches, boas
+    return x, a, A, entry, queries, searches, boas, warms

@@ -286,7 +286,7 @@ def test_split_all_or_no_survivors(tiny, eps):
 def test_hand_traced_golden():
     import os
     from helpers import load_beam_trace
-    x, a, adj, entry, queries, searches, boas = load_beam_trace(
+    x, a, adj, entry, queries, searches, boas, _ = load_beam_trace(
         os.path.join(os.path.dirname(__file__), "golden", "beam_trace.txt"))
     gpu = _boa().Index(x, a, np.zeros(1, np.int32), adj, entry)
     for c in searches:

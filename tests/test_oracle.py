@@ -216,7 +216,7 @@ _TRACE = load_beam_trace(os.path.join(GOLDEN, "beam_trace.txt"))
 
 
 def _trace_index():
-    x, a, adj, entry, _, _, _ = _TRACE
+    x, a, adj, entry = _TRACE[:4]
     return oracle.Index(x, a, np.zeros(1, np.int32), adj, entry)
 
 
@@ -242,6 +242,79 @@ def test_boa_matches_hand_trace(case):
     assert res.ids[0, :n].tolist() == case["ids"] and (res.ids[0, n:] == PAD).all()
     assert res.dists[0, :n].tolist() == case["d"]
     assert (res.final_L[0], res.expansions[0], res.scored[0]) == (case["final_L"], case["E"], case["S"])
+
+
+# ---------------------------------------------------------------------------
+# warm-start escalation (Sec. III-A "Redundancy Avoidance"; reading in the
+# oracle's orc_boa_warm): hand-traced cases, and what the reading fixes
+
+@pytest.mark.parametrize("case", _TRACE[7], ids=lambda c: f"{c['q']}-k{c['k']}-warm")
+def test_warm_matches_hand_trace(case):
+    ix = _trace_index()
+    q, r = _TRACE[4][case["q"]]
+    res = oracle.boa_warm(ix, q, r, case["k"], case["widths"], eps=case["eps"])
+    n = len(case["ids"])
+    assert res.ids[0, :n].tolist() == case["ids"] and (res.ids[0, n:] == PAD).all()
+    assert res.dists[0, :n].tolist() == case["d"]
+    assert (res.final_L[0], res.expansions[0], res.scored[0]) == (case["final_L"], case["E"], case["S"])
+
+
+def test_warm_first_phase_is_the_restart_search(mid_index):
+    """Phase 0 of the warm mode keeps a longer list but expands only among
+    its first L0 entries: its worklist, and so every query that settles
+    there, equal the fresh width-L0 search (results, E and S)."""
+    ix = mid_index
+    q, r = random_queries(ix, 60, 30, seed=41, f32_col=True)
+    sched = oracle.schedule(10, 2.0, 160)
+    # k = 5 < L0: a width-10 worklist can hold more valid entries than k,
+    # so queries can settle at the first width (n_valid <= k never does)
+    warm = oracle.boa_warm(ix, q, r, 5, sched, eps=0.3)
+    cold = oracle.boa(ix, q, r, 5, sched, eps=0.3)
+    assert warm.phases[0] == cold.phases[0]
+    first = cold.final_L == sched[0]
+    assert first.any() and (~first).any()
+    np.testing.assert_array_equal(warm.final_L[first], cold.final_L[first])
+    for a, b in ((warm.ids, cold.ids), (warm.dists, cold.dists), (warm.expansions, cold.expansions),
+                 (warm.scored, cold.scored)):
+        np.testing.assert_array_equal(a[first], b[first])
+    # the escalated ones stop at the same widths (the test sees each phase's
+    # worklist) only by coincidence; but they never score a node twice: at
+    # most every point once over all phases
+    assert (warm.scored <= ix.n).all()
+    assert (warm.scored[~first] < cold.scored[~first]).mean() > 0.5
+
+
+def test_warm_two_widths_ending_at_n_is_exact():
+    """With widths [L0, N >= n] the first phase keeps up to N candidates,
+    so nothing is ever cut and the last phase expands every reachable
+    node: the result is the exact filtered top-k (Def. 1)."""
+    ix = random_index(n=300, d=16, m=2, R=10, seed=43, f32_col=True)
+    q, r = random_queries(ix, 15, 40, seed=43, f32_col=True)
+    res = oracle.boa_warm(ix, q, r, 10, [10, ix.n], eps=0.0)
+    bi, bd, nv = oracle.bruteforce(ix, q, r, 10)
+    esc = res.final_L == ix.n
+    assert esc.any()
+    np.testing.assert_array_equal(res.ids[esc], bi[esc])
+    np.testing.assert_array_equal(res.dists[esc], bd[esc])
+    assert (res.scored[esc] == ix.n).all()   # every node scored exactly once
+
+
+def test_warm_result_invariants(mid_index):
+    ix = mid_index
+    q, r = random_queries(ix, 50, 25, seed=44, f32_col=True)
+    sched = oracle.schedule(16, 2.0, 256)
+    res = oracle.boa_warm(ix, q, r, 10, sched, eps=0.05)
+    for i in range(q.shape[0]):
+        assert res.final_L[i] in sched
+        got = res.ids[i][res.ids[i] != PAD]
+        assert numpy_valid(ix, r[i])[got.astype(np.int64)].all()
+        dd = res.dists[i][:len(got)]
+        assert list(zip(dd, got)) == sorted(zip(dd, got))
+        assert len(set(got.tolist())) == len(got)
+        for j, g in enumerate(got):
+            assert dd[j] == oracle.dist(ix.vectors[g], q[i])
+    assert sum(p["expansions"] for p in res.phases) == res.expansions.sum()
+    assert sum(p["scored"] for p in res.phases) == res.scored.sum()
 
 
 # ---------------------------------------------------------------------------
