@@ -130,6 +130,15 @@ typedef struct {
                                survivors run at once (identical results; needs
                                tau == 0). 0: one launch per phase with device-side
                                compaction between them. */
+    int32_t warm_start;     /* 1: warm-start escalation (Sec. III-A "Redundancy
+                               Avoidance"): during a phase of width L the sorted list
+                               keeps up to the next phase's width, only its first L
+                               entries are expanded and read by the result and Eq. 3,
+                               and an escalated query continues from that list and its
+                               visited set instead of restarting at the entry point.
+                               The first phase is unchanged; later phases differ from a
+                               restart. Runs in the fused mode only (fused = 1, so
+                               tau == 0), else BOA_EUNSUPPORTED. 0: every phase restarts. */
 } boa_params;
 
 void boa_default_params(boa_params *p);

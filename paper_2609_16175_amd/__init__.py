@@ -38,7 +38,8 @@ class Params(C.Structure):
     _fields_ = [("k", C.c_int32), ("L0", C.c_int32), ("Lmax", C.c_int32), ("alpha", C.c_double),
                 ("eps", C.c_double), ("tau", C.c_double), ("fixed_L", C.c_int32),
                 ("boa_plus", C.c_int32), ("sub_batches", C.c_int32), ("lds_hash_slots", C.c_int32),
-                ("schedule", C.POINTER(C.c_int32)), ("n_schedule", C.c_int32), ("fused", C.c_int32)]
+                ("schedule", C.POINTER(C.c_int32)), ("n_schedule", C.c_int32), ("fused", C.c_int32),
+                ("warm_start", C.c_int32)]
 
 
 class PhaseStats(C.Structure):
@@ -169,13 +170,18 @@ class Index:
                eps: float = 0.05, tau: float = 0.0, fixed_L: int = 0, boa_plus: bool = False,
                sub_batches: int = 10, lds_hash_slots: int = 0, schedule=None, fused: bool = False,
                split: bool = False, counters: bool = False,
-               stream=None, out=None, no_alloc: bool = False) -> SearchResult:
+               stream=None, out=None, no_alloc: bool = False, warm: bool = False) -> SearchResult:
         """Adaptive filtered top-k of a batch of device-resident queries.
 
         queries: torch tensor (nq, d) on the GPU, float32 or uint8 like the index.
         ranges:  torch int32 tensor (nq, m, 2) on the GPU (float32 columns as bit patterns).
         fused:   every phase in one persistent launch; split: the first phase in
                  one launch, the survivors through all later phases in a second.
+        warm:    warm-start escalation (fused mode): each phase continues from
+                 the previous phase's list and visited set.
+        no_alloc: call boa_search_noalloc (the library allocates no device
+                 memory for the call; pass preallocated `out` tensors to
+                 allocate nothing on the torch side either).
         """
         import torch
         if not (queries.is_cuda and ranges.is_cuda):
@@ -203,6 +209,7 @@ class Index:
         if fused and split:
             raise ValueError("fused and split are exclusive")
         p.fused = 2 if split else int(fused)
+        p.warm_start = int(warm)
         sched_arr = None
         if schedule is not None:
             sched_arr = (C.c_int32 * len(schedule))(*schedule)

@@ -574,7 +574,7 @@ struct Workspace {
 struct Request {
     int32_t sched[BOA_MAX_PHASES];
     int32_t n_phases;
-    bool plus, split, fused;
+    bool plus, split, fused, warm;
     int32_t sub;              // BOA+ sub-batches (1 otherwise)
     int32_t n_counters;
     uint32_t tau_count;
@@ -609,6 +609,10 @@ int validate(const boa_index *ix, const void *queries, const int32_t *ranges, in
     if (rq.plus && p->tau != 0.0)
         return fail(BOA_EINVAL, "BOA+ needs tau == 0 (the residual test counts all queries of a phase)");
     if (rq.plus && (p->sub_batches < 1 || p->sub_batches > 1024)) return fail(BOA_EINVAL, "sub_batches out of range");
+    if (p->warm_start != 0 && p->warm_start != 1) return fail(BOA_EINVAL, "warm_start must be 0 or 1");
+    if (p->warm_start && !rq.fused)
+        return fail(BOA_EUNSUPPORTED, "warm-start escalation runs in the fused mode (fused = 1)");
+    rq.warm = p->warm_start == 1;
     rq.sub = rq.plus ? std::min<int64_t>(p->sub_batches, std::max<int64_t>(nq, 1)) : 1;
     rq.n_counters = rq.n_phases * (rq.sub + 1) + 8;
     rq.tau_count = (uint32_t)std::floor(p->tau * (double)nq);
@@ -731,6 +735,7 @@ int run_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_
         a.queue = ws.counters;
         a.p_begin = 0;
         a.p_end = n_phases;
+        a.warm = rq.warm ? 1 : 0;
         a.L_alloc = Lw;
         a.h_log2 = ilog2((uint32_t)pl.h_slots);
         a.lds_per_wave = pl.lds_per_wave;

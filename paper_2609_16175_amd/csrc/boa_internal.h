@@ -49,6 +49,7 @@ struct PhaseArgs {
     int32_t sched[BOA_MAX_PHASES]; // phase widths
     int32_t p_begin, p_end;   // phases run by this launch (one, or all when fused)
     int32_t write_conf;       // record each query's confidence for a compaction/append
+    int32_t warm;             // warm-start escalation: phases continue from the previous one's state
     int32_t L_alloc;          // widest of them: sizes the per-wave LDS
     int32_t h_log2;           // log2 of the LDS visited-table slots (16-bit entries)
     int32_t vis_bitmap;       // 1: the visited set is instead an LDS bitmap over all n ids

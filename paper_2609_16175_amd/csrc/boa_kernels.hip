@@ -525,16 +525,25 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         }
         // the phases of this launch: each restarts the search from the entry
         // point at its own width (Alg. 1 calls Alg. 2 afresh)
+        // search state; in the warm-start mode it carries over from phase to
+        // phase (the worklist, its expanded flags and the visited set)
+        bool spill = false;
+        uint32_t len = 0;
         for (int p = a.p_begin; p < a.p_end; ++p) {
         const int L = a.sched[p];
-        {
+        // warm start: the list keeps up to the next phase's width while only
+        // its first L entries are expanded (the last phase keeps L)
+        const int Lcap = (a.warm && p + 1 < a.p_end) ? a.sched[p + 1] : L;
+        const bool fresh = !a.warm || p == a.p_begin;
+        if (fresh) {
             uint4 z = make_uint4(0, 0, 0, 0);
             uint4 *h4 = reinterpret_cast<uint4 *>(htab);
             for (uint32_t i = lane; i < table_words >> 2; i += 64) h4[i] = z;
+            spill = false;
+            len = 0;
         }
         wave_sync();
 
-        bool spill = false;
         // test-and-insert of this lane's neighbour: 1 new, 0 seen (or padding)
         auto visit_test = [&](uint32_t v) -> int {
             if (a.vis_bitmap) {   // one bit per id: a single LDS atomic
@@ -554,7 +563,6 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             return vst;
         };
         uint32_t E = 0, S = 0;
-        uint32_t len = 0;
         int expanded_j = -1;
         // adjacency row already in flight for the node expected next
         uint32_t pf_id = BOA_PAD;
@@ -562,8 +570,9 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         uint32_t pf_row = BOA_PAD;
 
         // the entry point is scored and entered before the first expansion
-        uint32_t c = 1;
-        if (lane == 0) {
+        // (a warm phase continues with nothing new to score)
+        uint32_t c = fresh ? 1u : 0u;
+        if (fresh && lane == 0) {
             if (a.vis_bitmap) htab[ix.entry >> 5] |= 1u << (ix.entry & 31u);
             else visit_lds(vs, ix.entry);
             cid[0] = ix.entry;
@@ -594,7 +603,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                 }
                 PROF_T(t_score1);
                 PROF_ADD(2, t_score1 - t_score0);
-                if (len == (uint32_t)L && key >= beam[L - 1]) key = KEY_NONE;  // cannot enter
+                if (len == (uint32_t)Lcap && key >= beam[Lcap - 1]) key = KEY_NONE;  // cannot enter
                 const uint64_t keep = __ballot(key != KEY_NONE);
                 const uint32_t kept = __popcll(keep);
                 if (kept > 0) {
@@ -643,11 +652,11 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                         f = pos + lane;
                     }
                     const uint32_t p0 = bcast0(pos);
-                    const uint32_t newlen = min((uint32_t)L, len + kept);
+                    const uint32_t newlen = min((uint32_t)Lcap, len + kept);
                     const uint32_t w_lo = p0 >> 6, w_hi = (newlen - 1u) >> 6;
                     for (uint32_t w = w_lo + lane; w <= w_hi; w += 64) posbm[w] = 0ull;
                     wave_sync();
-                    const bool placed = f < (uint32_t)L;
+                    const bool placed = f < (uint32_t)Lcap;
                     if (placed) atomicOr(reinterpret_cast<unsigned long long *>(&posbm[f >> 6]),
                                          1ull << (f & 63u));
                     const uint32_t n_placed = __popcll(__ballot(placed));
@@ -681,12 +690,14 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             }
             PROF_T(t_sel0);
 
-            // ---- select the nearest unexpanded entry (and predict the one after it)
+            // ---- select the nearest unexpanded entry among the first L (and
+            // predict the one after it)
+            const uint32_t lim = min(len, (uint32_t)L);
             int j = -1, j2 = -1;
             uint64_t ku = 0, kn = KEY_NONE;   // their keys, taken from the lanes that read them
-            for (uint32_t b0 = scan_from; b0 < len; b0 += 64) {
+            for (uint32_t b0 = scan_from; b0 < lim; b0 += 64) {
                 const uint32_t i = b0 + lane;
-                const uint64_t bk = i < len ? beam[i] : 1ull;
+                const uint64_t bk = i < lim ? beam[i] : 1ull;
                 const uint64_t mk = __ballot(!(bk & 1ull));
                 if (mk) {
                     const int l1 = __ffsll((unsigned long long)mk) - 1;
@@ -748,10 +759,11 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             PROF_ADD(6, spill ? 1 : 0);
         }
 
-        // ---- epilogue: confidence (Eq. 3); the result is written by the
-        // last phase the query runs in this launch
+        // ---- epilogue: confidence (Eq. 3) over the phase's worklist (its
+        // first L entries); the result is written by the last phase the
+        // query runs in this launch
         wave_sync();
-        const uint32_t n_valid = lower_bound64(beam, len, KEY_PHI1);
+        const uint32_t n_valid = lower_bound64(beam, min(len, (uint32_t)L), KEY_PHI1);
         const int k = a.k;
         uint32_t conf = 0;
         if (n_valid > (uint32_t)k) {

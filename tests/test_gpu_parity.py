@@ -286,7 +286,7 @@ def test_split_all_or_no_survivors(tiny, eps):
 def test_hand_traced_golden():
     import os
     from helpers import load_beam_trace
-    x, a, adj, entry, queries, searches, boas, _ = load_beam_trace(
+    x, a, adj, entry, queries, searches, boas, warms = load_beam_trace(
         os.path.join(os.path.dirname(__file__), "golden", "beam_trace.txt"))
     gpu = _boa().Index(x, a, np.zeros(1, np.int32), adj, entry)
     for c in searches:
@@ -305,4 +305,68 @@ def test_hand_traced_golden():
             assert ids[0, :n].tolist() == c["ids"] and (ids[0, n:] == PAD).all(), (c, mode)
             assert dists[0, :n].tolist() == c["d"], (c, mode)
             assert (fl[0], E[0], S[0]) == (c["final_L"], c["E"], c["S"]), (c, mode)
+    for c in warms:
+        q, r = queries[c["q"]]
+        ids, dists, fl, E, S = gpu_search(gpu, q, r, k=c["k"], schedule=c["widths"], eps=c["eps"],
+                                          fused=True, warm=True)
+        n = len(c["ids"])
+        assert ids[0, :n].tolist() == c["ids"] and (ids[0, n:] == PAD).all(), c
+        assert dists[0, :n].tolist() == c["d"], c
+        assert (fl[0], E[0], S[0]) == (c["final_L"], c["E"], c["S"]), c
     gpu.close()
+
+
+# ---------------------------------------------------------------------------
+# warm-start escalation (fused mode) against the oracle's mirror mode
+
+@pytest.mark.parametrize("eps", [0.0, 0.02, 0.05, 0.2])
+def test_tiny_warm(tiny, eps):
+    wl, d = tiny["wl"], tiny["data"]
+    sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
+    ref = oracle.boa_warm(tiny["orc"], d.queries, d.ranges, wl.k, sched, eps=eps)
+    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax, eps=eps,
+                     fused=True, warm=True)
+    assert_parity(got, ref, f"tiny warm eps={eps}")
+    st = tiny["gpu"].stats()
+    for p, rp in zip(st["phases"], ref.phases):
+        assert (p["active"], p["confident"], p["expansions"], p["scored"]) == \
+            (rp["active"], rp["confident"], rp["expansions"], rp["scored"])
+
+
+@pytest.mark.parametrize("slots", [64, 256])
+def test_warm_forced_spill(tiny, slots):
+    """The visited set carried from phase to phase, with most inserts in the
+    HBM bitmap (which must then not be reset by a continuing phase)."""
+    wl, d = tiny["wl"], tiny["data"]
+    sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
+    ref = oracle.boa_warm(tiny["orc"], d.queries, d.ranges, wl.k, sched, eps=0.01)
+    got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax, eps=0.01,
+                     fused=True, warm=True, lds_hash_slots=slots)
+    assert_parity(got, ref, f"warm spill slots={slots}")
+    assert tiny["gpu"].stats()["spilled_queries"] > 0
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=[f"{s[0]}-d{s[1]}-m{s[2]}-R{s[3]}" for s in SHAPES])
+def test_shapes_warm(shape):
+    dtype, d, m, R, f32col = shape
+    boa = _boa()
+    arrs = random_arrays(n=3000, d=d, m=m, R=R, dtype=dtype, seed=d + m + R, f32_col=f32col)
+    orc = oracle.Index(*arrs)
+    gpu = boa.Index(*arrs)
+    q, r = random_queries(orc, 150, 40, seed=d, f32_col=f32col)
+    for sched in (oracle.schedule(16, 2.0, 256), [10, 100, 200]):
+        ref = oracle.boa_warm(orc, q, r, 10, sched, eps=0.05)
+        got = gpu_search(gpu, q, r, k=10, schedule=sched, eps=0.05, fused=True, warm=True)
+        assert_parity(got, ref, f"shape {shape} warm {sched}")
+    gpu.close()
+
+
+def test_warm_needs_the_fused_mode(tiny):
+    boa = _boa()
+    wl, d = tiny["wl"], tiny["data"]
+    q = torch.from_numpy(d.queries[:4]).to("cuda:0")
+    r = torch.from_numpy(d.ranges[:4]).to("cuda:0")
+    for mode in ({}, {"split": True}, {"boa_plus": True}):
+        with pytest.raises(boa.BoaError) as e:
+            tiny["gpu"].search(q, r, k=wl.k, warm=True, **mode)
+        assert e.value.code == -4
