@@ -365,38 +365,64 @@ def main():
     # the target there (split mode, a few steps each)
     eps_grid = [args.eps] if args.eps > 0 else [float(x) for x in args.eps_grid.split(",")]
     alpha_grid = [args.alpha] if args.alpha > 0 else [float(x) for x in args.alpha_grid.split(",")]
-    points = [(e, a) for a in alpha_grid for e in eps_grid]
+    # two kinds of escalation: each phase restarting the search (Alg. 1 as
+    # printed; timed in split mode here) or continuing from the previous
+    # phase's state (warm start, fused mode)
+    kinds = {"restart": {"split": True}, "warm": {"fused": True, "warm": True}}
+    points = [(e, a, kd) for kd in kinds for a in alpha_grid for e in eps_grid]
     sweep = []
-    for e, a in points:
-        ms_p, st_p, o_p = timed(dict(base_kw, eps=e, alpha=a, split=True), 3, 1, q_ho, r_ho)
+    for e, a, kd in points:
+        ms_p, st_p, o_p = timed(dict(base_kw, eps=e, alpha=a, **kinds[kd]), 3, 1, q_ho, r_ho)
         fl_p = o_p.final_L.cpu().numpy()
         _, rt_p = eval_recall(o_p, heldout=True)
-        sweep.append(dict(eps=e, alpha=a, schedule=[p["L"] for p in st_p["phases"]],
+        sweep.append(dict(eps=e, alpha=a, escalation=kd, schedule=[p["L"] for p in st_p["phases"]],
                           ms_per_step=round(ms_p, 4), qps=round(wl.nq / (ms_p / 1e3), 1),
                           recall_at_10=round(rt_p, 5), L_avg=round(float(fl_p.mean()), 2)))
-        log(f"held-out point eps={e} alpha={a}: {ms_p:.3f} ms/step (split), recall {rt_p:.4f}, "
+        log(f"held-out point eps={e} alpha={a} {kd}: {ms_p:.3f} ms/step, recall {rt_p:.4f}, "
             f"L_avg {fl_p.mean():.1f}")
-    ok = [p for p in sweep if p["recall_at_10"] >= args.recall_target]
-    chosen = min(ok, key=lambda p: p["ms_per_step"]) if ok else max(sweep, key=lambda p: p["recall_at_10"])
-    log(f"chosen on the held-out batch: eps={chosen['eps']} alpha={chosen['alpha']} "
-        f"({'meets' if ok else 'MISSES'} recall@10 >= {args.recall_target} there)")
-    kw = dict(base_kw, eps=chosen["eps"], alpha=chosen["alpha"])
 
-    modes = {}
+    def choose(pts):
+        ok = [p for p in pts if p["recall_at_10"] >= args.recall_target]
+        return (min(ok, key=lambda p: p["ms_per_step"]) if ok else max(pts, key=lambda p: p["recall_at_10"])), bool(ok)
+
+    chosen, _ = choose(sweep)
+    chosen_kind = {kd: choose([p for p in sweep if p["escalation"] == kd])[0] for kd in kinds}
+    log(f"chosen on the held-out batch: eps={chosen['eps']} alpha={chosen['alpha']} {chosen['escalation']} "
+        f"({'meets' if chosen['recall_at_10'] >= args.recall_target else 'MISSES'} recall@10 >= "
+        f"{args.recall_target} there)")
+
+    # every restart mode at the restart kind's point (identical results), the
+    # warm mode at the warm kind's point; the headline is the chosen kind's
+    # fastest mode
     mode_kw = {"phased": {}, "fused": {"fused": True}, "split": {"split": True},
-               "boa_plus": {"boa_plus": True, "sub_batches": wl.sub_batches}}
-    for mode in args.modes.split(","):
-        ms_m, st_m, out_m = timed(dict(kw, **mode_kw[mode]), args.steps, args.warmup)
+               "boa_plus": {"boa_plus": True, "sub_batches": wl.sub_batches},
+               "warm": {"fused": True, "warm": True}}
+    kw_kind = {kd: dict(base_kw, eps=c["eps"], alpha=c["alpha"]) for kd, c in chosen_kind.items()}
+    modes = {}
+    for mode in args.modes.split(",") + ["warm"]:
+        kd = "warm" if mode == "warm" else "restart"
+        ms_m, st_m, out_m = timed(dict(kw_kind[kd], **mode_kw[mode]), args.steps, args.warmup)
         modes[mode] = (ms_m, st_m, out_m)
-        log(f"adaptive ({mode}): {ms_m:.3f} ms/step, {wl.nq / (ms_m / 1e3):,.0f} QPS")
-    mode = min(modes, key=lambda k2: modes[k2][0])
+        log(f"adaptive ({mode}, eps={kw_kind[kd]['eps']} alpha={kw_kind[kd]['alpha']}): {ms_m:.3f} ms/step, "
+            f"{wl.nq / (ms_m / 1e3):,.0f} QPS")
+    restart_modes = [m2 for m2 in modes if m2 != "warm"]
+    ids_r = modes[restart_modes[0]][2].ids.cpu().numpy().view(np.uint32)
+    for m2 in restart_modes:
+        assert np.array_equal(modes[m2][2].ids.cpu().numpy().view(np.uint32), ids_r), f"{m2} results differ"
+    mode = "warm" if chosen["escalation"] == "warm" else min(restart_modes, key=lambda k2: modes[k2][0])
+    kw = kw_kind[chosen["escalation"]]
     ms, st, out = modes[mode]
     qps = wl.nq / (ms / 1e3)
+    other = "restart" if mode == "warm" else "warm"
+    om = "warm" if other == "warm" else min(restart_modes, key=lambda k2: modes[k2][0])
+    rs_o, rt_o = eval_recall(modes[om][2])
+    other_kind = dict(escalation=other, mode=om, eps=kw_kind[other]["eps"], alpha=kw_kind[other]["alpha"],
+                      ms_per_step=round(modes[om][0], 4), qps=round(wl.nq / (modes[om][0] / 1e3), 1),
+                      recall_at_10=round(rt_o, 5), recall_at_10_strict=round(rs_o, 5),
+                      L_avg=round(float(modes[om][2].final_L.cpu().numpy().mean()), 2))
 
     ids = out.ids.cpu().numpy().view(np.uint32)
     final_L = out.final_L.cpu().numpy()
-    for m2, (_, _, o2) in modes.items():
-        assert np.array_equal(o2.ids.cpu().numpy().view(np.uint32), ids), f"{m2} results differ"
     rec_strict, rec_tie = eval_recall(out)
     target_met = rec_tie >= args.recall_target
     sched = [p["L"] for p in st["phases"]]
@@ -440,7 +466,7 @@ def main():
     groups = []
     for gi, i in enumerate(starts):
         j = starts[gi + 1] if gi + 1 < len(starts) else nph
-        if mode == "fused":
+        if mode in ("fused", "warm"):
             j = nph
         nl = st["cum_phase_launches"][i]
         kms = st["cum_phase_kernel_ms"][i] / nl
@@ -488,15 +514,24 @@ def main():
 
     # the paper's own point (eps 0.05, alpha 2; Sec. IV), on the evaluation
     # batch, in the fastest mode
-    msp, stp, out_p = timed(dict(base_kw, eps=0.05, alpha=2.0, **mode_kw[mode]), args.fixed_steps, 1)
+    pmode = min(restart_modes, key=lambda k2: modes[k2][0])
+    msp, stp, out_p = timed(dict(base_kw, eps=0.05, alpha=2.0, **mode_kw[pmode]), args.fixed_steps, 1)
     rps, rpt = eval_recall(out_p)
-    paper_point = dict(eps=0.05, alpha=2.0, mode=mode, schedule=[p["L"] for p in stp["phases"]],
+    paper_point = dict(eps=0.05, alpha=2.0, mode=pmode, schedule=[p["L"] for p in stp["phases"]],
                        ms_per_step=round(msp, 4), qps=round(wl.nq / (msp / 1e3), 1), recall_at_10=round(rpt, 5),
                        recall_at_10_strict=round(rps, 5),
                        L_avg=round(float(out_p.final_L.cpu().numpy().mean()), 2),
                        speedup_vs_fixed_L500=round((wl.nq / (msp / 1e3)) / fixed["qps"], 3)
                        if fixed else None)
-    log(f"paper's point eps=0.05 alpha=2 ({mode}): {msp:.3f} ms/step, recall {rpt:.4f}")
+    log(f"paper's point eps=0.05 alpha=2 ({pmode}): {msp:.3f} ms/step, recall {rpt:.4f}")
+    # the same point with warm-start escalation
+    msw, _, out_w = timed(dict(base_kw, eps=0.05, alpha=2.0, **mode_kw["warm"]), args.fixed_steps, 1)
+    _, rwt = eval_recall(out_w)
+    paper_point["warm"] = dict(ms_per_step=round(msw, 4), qps=round(wl.nq / (msw / 1e3), 1),
+                               recall_at_10=round(rwt, 5),
+                               L_avg=round(float(out_w.final_L.cpu().numpy().mean()), 2),
+                               speedup_vs_fixed_L500=round((wl.nq / (msw / 1e3)) / fixed["qps"], 3) if fixed else None)
+    log(f"paper's point with warm start: {msw:.3f} ms/step, recall {rwt:.4f}")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -507,23 +542,44 @@ def main():
         threads = max(1, min(16, ci["affinity"]))
         oix = oracle.Index(data.vectors, data.attrs, types, adj, entry)
         osched = oracle.schedule(wl.L0, chosen["alpha"], wl.Lmax)
+
+        def run_oracle(n_q, nt):
+            """the oracle of the chosen escalation on the first n_q queries,
+            nt threads over independent queries"""
+            if chosen["escalation"] != "warm":
+                return oracle.boa(oix, data.queries[:n_q], data.ranges[:n_q], wl.k, osched, eps=chosen["eps"],
+                                  threads=nt)
+            from concurrent.futures import ThreadPoolExecutor
+            cuts = np.linspace(0, n_q, nt + 1).astype(int)
+            with ThreadPoolExecutor(nt) as ex:
+                parts = list(ex.map(lambda ab: oracle.boa_warm(oix, data.queries[ab[0]:ab[1]],
+                                                               data.ranges[ab[0]:ab[1]], wl.k, osched,
+                                                               eps=chosen["eps"]),
+                                    [(a, b) for a, b in zip(cuts[:-1], cuts[1:]) if b > a]))
+            return type(parts[0])(np.concatenate([p_.ids for p_ in parts]),
+                                  np.concatenate([p_.dists for p_ in parts]),
+                                  np.concatenate([p_.final_L for p_ in parts]),
+                                  np.concatenate([p_.expansions for p_ in parts]),
+                                  np.concatenate([p_.scored for p_ in parts]), [])
+
         # calibrate, then size the sample to the time budget
         n0 = min(wl.nq, 4 * threads)
         tc = time.perf_counter()
-        oracle.boa(oix, data.queries[:n0], data.ranges[:n0], wl.k, osched, eps=chosen["eps"], threads=threads)
+        run_oracle(n0, threads)
         per_q = (time.perf_counter() - tc) / n0
         ns = int(min(wl.nq, max(n0, args.cpu_seconds / max(per_q, 1e-6))))
         tc = time.perf_counter()
-        ref = oracle.boa(oix, data.queries[:ns], data.ranges[:ns], wl.k, osched, eps=chosen["eps"], threads=threads)
+        ref = run_oracle(ns, threads)
         el = time.perf_counter() - tc
         same = int(((ref.ids == ids[:ns]).all(1) & (ref.final_L == final_L[:ns])).sum())
         # the oracle on one thread as well (a smaller sample of the same queries)
         n1 = int(min(ns, max(1, (args.cpu_seconds / 3.0) / max(el * threads / ns, 1e-6))))
         tc = time.perf_counter()
-        oracle.boa(oix, data.queries[:n1], data.ranges[:n1], wl.k, osched, eps=chosen["eps"], threads=1)
+        run_oracle(n1, 1)
         el1 = time.perf_counter() - tc
         cpu = dict(value=round(ns / el, 2), unit="queries/s", cores=threads, kind="oracle",
-                   sample=f"first {ns} of {wl.nq} queries, full adaptive schedule, {threads} threads, "
+                   sample=f"first {ns} of {wl.nq} queries, full adaptive schedule "
+                          f"({chosen['escalation']} escalation), {threads} threads, "
                           f"{el:.1f}s wall",
                    one_thread_value=round(n1 / el1, 2), one_thread_sample=f"first {n1} queries, {el1:.1f}s wall",
                    cpu_model=ci.get("model"), sockets=ci.get("sockets"), nproc=ci["nproc"],
@@ -547,7 +603,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "n": wl.n, "d": wl.d, "R": wl.R, "m": wl.m, "nq": wl.nq,
                    "k": wl.k, "L0": wl.L0, "Lmax": wl.Lmax, "alpha": chosen["alpha"], "eps": chosen["eps"],
-                   "schedule": sched, "mode": f"BOA ({mode} phases)", "graph": recipe,
+                   "schedule": sched, "escalation": chosen["escalation"],
+                   "mode": f"BOA ({mode} phases)" if mode != "warm" else "BOA (warm-start escalation, fused)",
+                   "graph": recipe,
                    "operating_point_chosen_on": "held-out batch of the same recipe"},
         "modes": {m2: {"ms_per_step": round(v[0], 4), "qps": round(wl.nq / (v[0] / 1e3), 1),
                        "launches_per_step": round(v[1]["cum_launches"] / max(1, v[1]["cum_searches"]), 2)}
@@ -565,6 +623,7 @@ def main():
         "recall_target": args.recall_target,
         "recall_target_met": bool(target_met),
         "operating_points_heldout": sweep,
+        "other_escalation": other_kind,
         "paper_point": paper_point,
         "fixed_L500": fixed,
         "speedup_vs_fixed_L500": round(qps / fixed["qps"], 3) if fixed else None,
