@@ -77,13 +77,14 @@ enum { BOA_ATTR_I32 = 0, BOA_ATTR_F32 = 1 };
  *               0xFFFFFFFF; 1 <= R <= BOA_MAX_R. A row may not hold its own
  *               id, nor any id twice.
  *               NULL: the library builds the graph (Sec. II "Graph
- *               construction": DiskANN alpha-pruning, alpha = 1.2, of each
- *               point's min(2R, 128) exact nearest neighbours, then of its
- *               forward and reverse neighbours to R - 1 edges, then every
- *               point made reachable from the entry point through an in-edge
- *               from its nearest reachable candidate). Needs n <=
- *               BOA_MAX_BUILD_N (the candidates come from a brute-force
- *               scan), else BOA_EUNSUPPORTED.
+ *               construction"; boa_build_params): DiskANN alpha-pruning of
+ *               each point's min(2R, 128) exact nearest neighbours, then of
+ *               its forward and reverse neighbours; attribute-aware edges
+ *               from JAG-style threshold passes (R >= 8); every row leaves
+ *               one slot free, and every point is made reachable from the
+ *               entry point through an in-edge from its nearest reachable
+ *               candidate. Needs n <= BOA_MAX_BUILD_N (the candidates come
+ *               from brute-force scans), else BOA_EUNSUPPORTED.
  *   R           the row width, 1 <= R <= BOA_MAX_R: one neighbour per lane of
  *               a 64-wide wavefront.
  *   entry       the entry point s of every search (Alg. 2), 0 <= entry < n;
@@ -98,6 +99,29 @@ int boa_build_index_from_arrays(const void *vectors, int64_t n, int32_t d, int32
                                 const int32_t *attrs, int32_t m, const int32_t *attr_dtypes,
                                 const uint32_t *adjacency, int32_t R, int64_t entry,
                                 boa_index **out);
+
+/* Graph construction parameters (used when adjacency is NULL). */
+typedef struct {
+    double alpha;        /* pruning slack of DiskANN's dominance rule: v is dropped
+                            when a kept w has alpha * d(w, v) <= d(u, v) (Euclidean);
+                            1 <= alpha <= 4; default 1.2 */
+    int32_t attr_levels; /* attribute-aware passes (JAG threshold pruning, Sec. II
+                            "Graph construction"), 0..4; default 4. Level l keeps, for
+                            each point, R/8 alpha-pruned nearest vectors among the
+                            points whose attribute distance (the largest gap of
+                            per-column quantile ranks) is within the point's
+                            0.1% / 1% / 5% / 20% quantile of that distance to an evenly
+                            spaced sample of 4096 points. The vector-distance pass
+                            keeps the rest of the row but one slot. Needs R >= 8. */
+} boa_build_params;
+
+void boa_default_build_params(boa_build_params *bp);
+
+/* boa_build_index_from_arrays with explicit graph construction parameters
+ * (bp must not be NULL). */
+int boa_build_index_ex(const void *vectors, int64_t n, int32_t d, int32_t vec_dtype, const int32_t *attrs,
+                       int32_t m, const int32_t *attr_dtypes, const uint32_t *adjacency, int32_t R,
+                       int64_t entry, const boa_build_params *bp, boa_index **out);
 
 /* Search parameters (Alg. 1 inputs). boa_default_params fills the defaults. */
 typedef struct {

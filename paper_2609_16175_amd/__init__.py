@@ -42,6 +42,10 @@ class Params(C.Structure):
                 ("warm_start", C.c_int32)]
 
 
+class BuildParams(C.Structure):
+    _fields_ = [("alpha", C.c_double), ("attr_levels", C.c_int32)]
+
+
 class PhaseStats(C.Structure):
     _fields_ = [("L", C.c_int32), ("active", C.c_int32), ("confident", C.c_int32),
                 ("launches", C.c_int32), ("expansions", C.c_int64), ("scored", C.c_int64),
@@ -79,6 +83,11 @@ def lib():
         L.boa_get_stats.argtypes = [P, C.POINTER(Stats)]
         L.boa_reset_counters.restype = C.c_int
         L.boa_reset_counters.argtypes = [P]
+        L.boa_build_index_ex.restype = C.c_int
+        L.boa_build_index_ex.argtypes = [P, C.c_int64, C.c_int32, C.c_int32, P, C.c_int32, P,
+                                         P, C.c_int32, C.c_int64, C.POINTER(BuildParams), C.POINTER(P)]
+        L.boa_default_build_params.restype = None
+        L.boa_default_build_params.argtypes = [C.POINTER(BuildParams)]
         L.boa_get_graph.restype = C.c_int
         L.boa_get_graph.argtypes = [P, P, C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
         L.boa_free_index.restype = None
@@ -115,10 +124,10 @@ class Index:
     """A graph index resident in device memory (owned by libboa)."""
 
     def __init__(self, vectors: np.ndarray, attrs: np.ndarray, attr_dtypes, adjacency, entry: int = -1,
-                 R: int = 0):
+                 R: int = 0, alpha: float = 1.2, attr_levels: int = 4):
         """adjacency: n x R uint32 rows, or None to have the library build the
-        graph with R edges per row; entry: the entry point, or -1 for the
-        medoid (computed by the library)."""
+        graph with R edges per row (alpha, attr_levels: boa_build_params);
+        entry: the entry point, or -1 for the medoid (computed by the library)."""
         vectors = np.ascontiguousarray(vectors)
         if vectors.dtype == np.float32:
             vt = VEC_F32
@@ -139,9 +148,12 @@ class Index:
         if attrs.shape != (n, types.shape[0]):
             raise ValueError("shape mismatch between vectors and attributes")
         h = C.c_void_p()
-        _check(lib().boa_build_index_from_arrays(vectors.ctypes.data, n, d, vt, attrs.ctypes.data,
-                                                 types.shape[0], types.ctypes.data, aptr,
-                                                 width, int(entry), C.byref(h)))
+        bp = BuildParams()
+        lib().boa_default_build_params(C.byref(bp))
+        bp.alpha, bp.attr_levels = alpha, attr_levels
+        _check(lib().boa_build_index_ex(vectors.ctypes.data, n, d, vt, attrs.ctypes.data,
+                                        types.shape[0], types.ctypes.data, aptr,
+                                        width, int(entry), C.byref(bp), C.byref(h)))
         self._h = h
         self.n, self.d, self.m, self.R = n, d, types.shape[0], width
         self.vec_dtype = vt

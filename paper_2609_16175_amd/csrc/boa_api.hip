@@ -190,11 +190,31 @@ void boa_free_index(boa_index *ix)
     delete ix;
 }
 
+void boa_default_build_params(boa_build_params *bp)
+{
+    if (!bp) return;
+    std::memset(bp, 0, sizeof(*bp));
+    bp->alpha = 1.2;
+    bp->attr_levels = 4;
+}
+
 int boa_build_index_from_arrays(const void *vectors, int64_t n, int32_t d, int32_t vec_dtype,
                                 const int32_t *attrs, int32_t m, const int32_t *attr_dtypes,
                                 const uint32_t *adjacency, int32_t R, int64_t entry, boa_index **out)
 {
+    boa_build_params bp;
+    boa_default_build_params(&bp);
+    return boa_build_index_ex(vectors, n, d, vec_dtype, attrs, m, attr_dtypes, adjacency, R, entry, &bp, out);
+}
+
+int boa_build_index_ex(const void *vectors, int64_t n, int32_t d, int32_t vec_dtype, const int32_t *attrs,
+                       int32_t m, const int32_t *attr_dtypes, const uint32_t *adjacency, int32_t R, int64_t entry,
+                       const boa_build_params *bp, boa_index **out)
+{
     if (!out) return fail(BOA_EINVAL, "out is NULL");
+    if (!bp) return fail(BOA_EINVAL, "NULL build parameters");
+    if (!(bp->alpha >= 1.0 && bp->alpha <= 4.0)) return fail(BOA_EINVAL, "alpha must be in [1, 4]");
+    if (bp->attr_levels < 0 || bp->attr_levels > 4) return fail(BOA_EINVAL, "attr_levels must be in [0, 4]");
     *out = nullptr;
     if (!vectors || !attrs || !attr_dtypes) return fail(BOA_EINVAL, "NULL input array");
     if (n < 1 || n >= BOA_MAX_N) return fail(BOA_EINVAL, "n out of range [1, 2^24)");
@@ -285,7 +305,8 @@ int boa_build_index_from_arrays(const void *vectors, int64_t n, int32_t d, int32
     }
     if (!adjacency) {
         BuildStats bs{};
-        hipError_t e = build_graph(ix->d_vectors, n, d, vec_dtype, R, (uint32_t)entry, ix->d_adj, &bs);
+        hipError_t e = build_graph(ix->d_vectors, n, d, vec_dtype, R, (uint32_t)entry, attrs, m, f32_mask,
+                                   (float)bp->alpha, bp->attr_levels, ix->d_adj, &bs);
         if (e != hipSuccess) {
             boa_free_index(ix);
             return fail(e == hipErrorOutOfMemory ? BOA_ENOMEM : BOA_EHIP,

@@ -28,6 +28,7 @@
 #include <cmath>
 #include <cstring>
 #include <queue>
+#include <thread>
 #include <vector>
 
 #include "boa_internal.h"
@@ -41,7 +42,6 @@ static constexpr int KNN_ROWS_B = KNN_ROWS_W * KNN_WAVES;
 static constexpr int KNN_LIST = 128;      // top-K capacity per row
 static constexpr int KNN_BUF = 64;        // new-candidate buffer per row
 static constexpr int KNN_KC = 64;         // dimensions per staged column chunk
-static constexpr float PRUNE_ALPHA2 = 1.44f;   // alpha = 1.2, squared
 
 __device__ __forceinline__ uint64_t bkey(float d, uint32_t id)
 {
@@ -233,7 +233,23 @@ struct KnnArgs {
     int32_t K;
     uint32_t *cand;    // n x K ids (0xFFFFFFFF padded)
     float *cand_d;     // n x K squared distances
+    // attribute-threshold pass: only points within a row's threshold count
+    const int32_t *ranks;   // n x m quantile ranks (null: no filter)
+    const int32_t *thr;     // n thresholds in rank units
+    int32_t m;
 };
+
+// attribute distance of two points: the largest gap between their ranks
+// over the columns
+__device__ __forceinline__ int32_t rank_gap(const int32_t *ranks, int m, int64_t a, int64_t b)
+{
+    int32_t g = 0;
+    for (int j = 0; j < m; ++j) {
+        const int32_t t = ranks[a * m + j] - ranks[b * m + j];
+        g = max(g, t < 0 ? -t : t);
+    }
+    return g;
+}
 
 template <bool U8>
 __global__ void __launch_bounds__(256) knn_kernel(KnnArgs a)
@@ -374,7 +390,9 @@ __global__ void __launch_bounds__(256) knn_kernel(KnnArgs a)
             const int64_t row = row0 + r;
             if (row >= n) continue;   // uniform
             const float dd = U8 ? (float)(int32_t)(rnorm[r] + cnorm - 2u * acci[r]) : accf[r];
-            const uint64_t key = (colv && col != row) ? bkey(dd, (uint32_t)col) : BKEY_NONE;
+            bool within = colv && col != row;
+            if (a.ranks && within) within = rank_gap(a.ranks, a.m, row, col) <= a.thr[row];
+            const uint64_t key = within ? bkey(dd, (uint32_t)col) : BKEY_NONE;
             const uint64_t m = __ballot(key < thr[r]);
             if (m) {
                 if (bufn[r] + (uint32_t)__popcll(m) > (uint32_t)KNN_BUF) merge_row(r);
@@ -423,6 +441,7 @@ struct PruneArgs {
     const uint32_t *rev;
     int32_t R;
     int32_t budget;
+    float alpha2;      // the pruning slack alpha, squared (squared distances)
     uint32_t *out;     // n x R (0xFFFFFFFF padded)
 };
 
@@ -430,7 +449,7 @@ struct PruneArgs {
 // (at most `budget` ids), by the alpha-dominance rule. Lanes test each
 // candidate against all kept points at once.
 __device__ void alpha_prune(const BuildView &v, uint32_t u, const uint64_t *keys, int cnt, int budget,
-                            uint32_t *kept, uint32_t *out_row, int R, int lane)
+                            float alpha2, uint32_t *kept, uint32_t *out_row, int R, int lane)
 {
     int nk = 0;
     for (int c = 0; c < cnt && nk < budget; ++c) {
@@ -442,7 +461,7 @@ __device__ void alpha_prune(const BuildView &v, uint32_t u, const uint64_t *keys
         for (int j0 = 0; j0 < nk; j0 += 64) {
             const int j = j0 + lane;
             bool hit = false;
-            if (j < nk) hit = PRUNE_ALPHA2 * dist_ids(v, kept[j], cv) <= duv;
+            if (j < nk) hit = alpha2 * dist_ids(v, kept[j], cv) <= duv;
             if (__ballot(hit)) {
                 dom = true;
                 break;
@@ -477,7 +496,8 @@ __global__ void __launch_bounds__(256) prune_fwd_kernel(PruneArgs a)
     }
     wave_fence();
     bitonic256(keys, lane);
-    alpha_prune(a.v, (uint32_t)u, keys, min(a.K, 256), a.budget, kept_s[wid], a.out + (size_t)u * a.R, a.R, lane);
+    alpha_prune(a.v, (uint32_t)u, keys, min(a.K, 256), a.budget, a.alpha2, kept_s[wid], a.out + (size_t)u * a.R,
+                a.R, lane);
 }
 
 // Re-prune each point's forward row together with its reverse neighbours
@@ -532,7 +552,7 @@ __global__ void __launch_bounds__(256) prune_union_kernel(PruneArgs a)
         wave_fence();
         bitonic256(keys, lane);
     }
-    alpha_prune(a.v, (uint32_t)u, keys, 256, a.budget, kept_s[wid], a.out + (size_t)u * a.R, a.R, lane);
+    alpha_prune(a.v, (uint32_t)u, keys, 256, a.budget, a.alpha2, kept_s[wid], a.out + (size_t)u * a.R, a.R, lane);
 }
 
 __global__ void count_in_kernel(const uint32_t *adj, int64_t n, int R, uint32_t *indeg)
@@ -627,10 +647,98 @@ size_t knn_lds_bytes(int vec_dtype)
     return lists + (size_t)(KNN_KC / 4) * 64 * unit + (size_t)KNN_ROWS_B * (KNN_KC / 4) * unit;
 }
 
+namespace {
+
+// Quantile rank of every attribute cell within its column: the number of
+// strictly smaller values (equal values share a rank); float32 columns
+// compare as floats.
+std::vector<int32_t> column_ranks(const int32_t *attrs, int64_t n, int m, uint32_t f32_mask)
+{
+    std::vector<int32_t> rk((size_t)n * m);
+    std::vector<int64_t> ord((size_t)n);
+    for (int j = 0; j < m; ++j) {
+        const bool f = (f32_mask >> j) & 1u;
+        auto val = [&](int64_t i) -> double {
+            const int32_t c = attrs[(size_t)i * m + j];
+            if (!f) return (double)c;
+            float x;
+            std::memcpy(&x, &c, 4);
+            return (double)x;
+        };
+        for (int64_t i = 0; i < n; ++i) ord[i] = i;
+        std::sort(ord.begin(), ord.end(), [&](int64_t a, int64_t b) { return val(a) < val(b); });
+        int64_t r = 0;
+        for (int64_t t = 0; t < n; ++t) {
+            if (t > 0 && val(ord[t]) != val(ord[t - 1])) r = t;
+            rk[(size_t)ord[t] * m + j] = (int32_t)r;
+        }
+    }
+    return rk;
+}
+
+// Per point and level: the q-quantile of its attribute distance to an
+// evenly spaced sample of S points (ids floor(i n / S)).
+std::vector<int32_t> level_thresholds(const std::vector<int32_t> &rk, int64_t n, int m, const double *q, int levels)
+{
+    const int64_t S = std::min<int64_t>(4096, n);
+    std::vector<int64_t> smp((size_t)S);
+    for (int64_t i = 0; i < S; ++i) smp[i] = (i * n) / S;
+    std::vector<int32_t> thr((size_t)levels * n);
+    auto work = [&](int64_t u0, int64_t u1) {
+        std::vector<int32_t> g((size_t)S);
+        for (int64_t u = u0; u < u1; ++u) {
+            for (int64_t i = 0; i < S; ++i) {
+                int32_t x = 0;
+                for (int j = 0; j < m; ++j) {
+                    const int32_t t = rk[(size_t)u * m + j] - rk[(size_t)smp[i] * m + j];
+                    x = std::max(x, t < 0 ? -t : t);
+                }
+                g[i] = x;
+            }
+            for (int l = 0; l < levels; ++l) {
+                const int64_t idx = std::max<int64_t>(0, (int64_t)std::ceil(q[l] * (double)S) - 1);
+                std::nth_element(g.begin(), g.begin() + idx, g.end());
+                thr[(size_t)l * n + u] = g[idx];
+            }
+        }
+    };
+    const int nt = (int)std::max<unsigned>(1u, std::min<unsigned>(16u, std::thread::hardware_concurrency()));
+    std::vector<std::thread> th;
+    for (int t = 0; t < nt; ++t) th.emplace_back(work, n * t / nt, n * (t + 1) / nt);
+    for (auto &x : th) x.join();
+    return thr;
+}
+
+hipError_t knn_launch(const KnnArgs &ka, int vec_dtype, int64_t n)
+{
+    const size_t lds = knn_lds_bytes(vec_dtype);
+    const unsigned blocks = (unsigned)((n + KNN_ROWS_B - 1) / KNN_ROWS_B);
+    if (vec_dtype == BOA_VEC_U8) {
+        BTRY(hipFuncSetAttribute(reinterpret_cast<const void *>(knn_kernel<true>),
+                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+        hipLaunchKernelGGL(knn_kernel<true>, dim3(blocks), dim3(256), lds, 0, ka);
+    } else {
+        BTRY(hipFuncSetAttribute(reinterpret_cast<const void *>(knn_kernel<false>),
+                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+        hipLaunchKernelGGL(knn_kernel<false>, dim3(blocks), dim3(256), lds, 0, ka);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t build_graph(const void *d_vectors, int64_t n, int32_t d, int vec_dtype, int32_t R, uint32_t entry,
+                       const int32_t *h_attrs, int32_t m, uint32_t f32_mask, float alpha, int32_t attr_levels,
                        uint32_t *d_adj, BuildStats *stats)
 {
     const bool u8 = vec_dtype == BOA_VEC_U8;
+    const float alpha2 = alpha * alpha;
+    // budgets: each attribute level R/8 edges, the vector pass the rest but
+    // one (the free slot the connectivity repair may take)
+    static const double kLevelQ[4] = {0.001, 0.01, 0.05, 0.2};
+    const int levels = (h_attrs && m > 0 && R >= 8) ? std::min(attr_levels, 4) : 0;
+    const int b_lvl = std::max(1, R / 8);
+    const int budget = std::max(1, R - 1 - levels * b_lvl);
     const int K = (int)std::min<int64_t>(std::min(2 * R, KNN_LIST), n - 1);
     DevBuf norms;
     BuildView v{d_vectors, nullptr, n, d, u8 ? 1 : 0};
@@ -644,27 +752,15 @@ hipError_t build_graph(const void *d_vectors, int64_t n, int32_t d, int vec_dtyp
         BTRY(hipMemset(d_adj, 0xFF, (size_t)n * R * 4));
         return hipSuccess;
     }
-    // 2. candidates
+    // 2. candidates by vector distance
     DevBuf cand, cand_d;
     BTRY(cand.alloc((size_t)n * K * 4));
     BTRY(cand_d.alloc((size_t)n * K * 4));
     {
-        KnnArgs ka{v, K, cand.as<uint32_t>(), cand_d.as<float>()};
-        const size_t lds = knn_lds_bytes(vec_dtype);
-        const unsigned blocks = (unsigned)((n + KNN_ROWS_B - 1) / KNN_ROWS_B);
-        if (u8) {
-            BTRY(hipFuncSetAttribute(reinterpret_cast<const void *>(knn_kernel<true>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-            hipLaunchKernelGGL(knn_kernel<true>, dim3(blocks), dim3(256), lds, 0, ka);
-        } else {
-            BTRY(hipFuncSetAttribute(reinterpret_cast<const void *>(knn_kernel<false>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-            hipLaunchKernelGGL(knn_kernel<false>, dim3(blocks), dim3(256), lds, 0, ka);
-        }
-        BTRY(hipGetLastError());
+        KnnArgs ka{v, K, cand.as<uint32_t>(), cand_d.as<float>(), nullptr, nullptr, 0};
+        BTRY(knn_launch(ka, vec_dtype, n));
     }
-    // 3. forward prune to R - 1 (one slot kept for the repair)
-    const int budget = std::max(1, R - 1);
+    // 3. forward prune
     DevBuf fwd;
     BTRY(fwd.alloc((size_t)n * R * 4));
     {
@@ -674,6 +770,7 @@ hipError_t build_graph(const void *d_vectors, int64_t n, int32_t d, int vec_dtyp
         pa.K = K;
         pa.R = R;
         pa.budget = budget;
+        pa.alpha2 = alpha2;
         pa.out = fwd.as<uint32_t>();
         hipLaunchKernelGGL(prune_fwd_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, 0, pa);
         BTRY(hipGetLastError());
@@ -705,17 +802,67 @@ hipError_t build_graph(const void *d_vectors, int64_t n, int32_t d, int vec_dtyp
         pa.rev = rev.as<uint32_t>();
         pa.R = R;
         pa.budget = budget;
+        pa.alpha2 = alpha2;
         pa.out = d_adj;
         hipLaunchKernelGGL(prune_union_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, 0, pa);
         BTRY(hipGetLastError());
     }
-    // 5. connectivity repair from s (host): breadth-first search, then each
-    // unreached point (ascending id) gets an in-edge from its nearest
-    // reached kNN candidate with a free slot; the search then continues
-    // from it
     std::vector<uint32_t> adj((size_t)n * R), hc((size_t)n * K);
     BTRY(hipMemcpy(adj.data(), d_adj, adj.size() * 4, hipMemcpyDeviceToHost));
     BTRY(hipMemcpy(hc.data(), cand.p, hc.size() * 4, hipMemcpyDeviceToHost));
+    // 5. attribute-aware edges (JAG threshold pruning, Sec. II "Graph
+    // construction"): per level, the alpha-pruned nearest vectors among the
+    // points within the point's attribute threshold (where the capped
+    // attribute distance is zero), b_lvl edges each, appended to the row
+    int64_t attr_edges = 0;
+    if (levels > 0) {
+        const std::vector<int32_t> rk = column_ranks(h_attrs, n, m, f32_mask);
+        const std::vector<int32_t> thr = level_thresholds(rk, n, m, kLevelQ, levels);
+        const int Kl = (int)std::min<int64_t>(std::min(4 * b_lvl, KNN_LIST), n - 1);
+        DevBuf d_rk, d_thr, lc, lcd, lrow;
+        BTRY(d_rk.alloc(rk.size() * 4));
+        BTRY(d_thr.alloc((size_t)n * 4));
+        BTRY(lc.alloc((size_t)n * Kl * 4));
+        BTRY(lcd.alloc((size_t)n * Kl * 4));
+        BTRY(lrow.alloc((size_t)n * R * 4));
+        BTRY(hipMemcpy(d_rk.p, rk.data(), rk.size() * 4, hipMemcpyHostToDevice));
+        std::vector<uint32_t> hl((size_t)n * R);
+        for (int l = 0; l < levels; ++l) {
+            BTRY(hipMemcpy(d_thr.p, thr.data() + (size_t)l * n, (size_t)n * 4, hipMemcpyHostToDevice));
+            KnnArgs ka{v, Kl, lc.as<uint32_t>(), lcd.as<float>(), d_rk.as<int32_t>(), d_thr.as<int32_t>(), m};
+            BTRY(knn_launch(ka, vec_dtype, n));
+            PruneArgs pa{};
+            pa.v = v;
+            pa.cand = lc.as<uint32_t>();
+            pa.K = Kl;
+            pa.R = R;
+            pa.budget = b_lvl;
+            pa.alpha2 = alpha2;
+            pa.out = lrow.as<uint32_t>();
+            hipLaunchKernelGGL(prune_fwd_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, 0, pa);
+            BTRY(hipGetLastError());
+            BTRY(hipMemcpy(hl.data(), lrow.p, hl.size() * 4, hipMemcpyDeviceToHost));
+            for (int64_t u = 0; u < n; ++u) {
+                uint32_t *row = &adj[(size_t)u * R];
+                int cnt = 0;
+                while (cnt < R && row[cnt] != BOA_PAD) ++cnt;
+                for (int i = 0; i < b_lvl && cnt < R - 1; ++i) {
+                    const uint32_t x = hl[(size_t)u * R + i];
+                    if (x == BOA_PAD) break;
+                    bool dup = false;
+                    for (int t = 0; t < cnt; ++t) dup |= row[t] == x;
+                    if (!dup) {
+                        row[cnt++] = x;
+                        ++attr_edges;
+                    }
+                }
+            }
+        }
+    }
+    // 6. connectivity repair from s (host): breadth-first search, then each
+    // unreached point (ascending id) gets an in-edge from its nearest
+    // reached kNN candidate with a free slot; the search then continues
+    // from it
     std::vector<uint8_t> seen((size_t)n, 0);
     std::vector<uint32_t> queue;
     queue.reserve((size_t)n);
@@ -752,8 +899,8 @@ hipError_t build_graph(const void *d_vectors, int64_t n, int32_t d, int vec_dtyp
             }
         }
         if (w < 0) {
-            // no reached candidate with room: the lowest reached id with a
-            // free slot (every row was pruned to at most R - 1 edges)
+            // no reached candidate with room: the first reached point (in
+            // search order) with a free slot (every row keeps one)
             for (size_t q = 0; q < queue.size() && w < 0; ++q)
                 if (free_slot(queue[q]) >= 0) w = queue[q];
             ++fallback;
@@ -768,6 +915,7 @@ hipError_t build_graph(const void *d_vectors, int64_t n, int32_t d, int vec_dtyp
         stats->K = K;
         stats->repaired = repaired;
         stats->repair_fallback = fallback;
+        stats->attr_edges = attr_edges;
         int64_t edges = 0;
         for (uint32_t x : adj) edges += x != BOA_PAD;
         stats->edges = edges;

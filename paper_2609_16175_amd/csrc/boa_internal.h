@@ -96,9 +96,13 @@ struct BuildStats {
     int64_t edges;             // edges of the final graph
     int64_t repaired;          // in-edges added to reach every point from s
     int64_t repair_fallback;   // of which not from the point's own candidates
+    int64_t attr_edges;        // edges from the attribute-threshold passes
 };
 hipError_t compute_medoid(const void *d_vectors, int64_t n, int32_t d, int vec_dtype, uint32_t *entry);
+// h_attrs: HOST n x m cells (float32 columns flagged in f32_mask), or null
+// for a graph from vector distances only
 hipError_t build_graph(const void *d_vectors, int64_t n, int32_t d, int vec_dtype, int32_t R, uint32_t entry,
+                       const int32_t *h_attrs, int32_t m, uint32_t f32_mask, float alpha, int32_t attr_levels,
                        uint32_t *d_adj, BuildStats *stats);
 
 // wide: the scorer variant with twice the rows in flight (for launches that

@@ -57,6 +57,42 @@ def _nn_rows_ok(x, adj, sample):
     return bad
 
 
+def _attr_level0_ok(attrs, types, x, adj, sample, q=0.001):
+    """The attribute-aware pass of the tightest level (JAG threshold
+    pruning): for each sampled point u, the nearest point (float64) among
+    those within u's attribute threshold is in u's row. The threshold is
+    recomputed here with numpy from its definition: ranks = number of
+    strictly smaller values per column (float32 columns as floats), the
+    attribute distance = the largest rank gap over the columns, the
+    threshold = the ceil(q S)-th smallest distance to the S = min(4096, n)
+    points floor(i n / S)."""
+    from workloads import gen
+    n, m = attrs.shape
+    rk = np.empty((n, m), dtype=np.int64)
+    for j in range(m):
+        col = gen.cells_as_f32(attrs[:, j]) if types[j] == gen.ATTR_F32 else attrs[:, j]
+        rk[:, j] = np.searchsorted(np.sort(col), col, side="left")
+    S = min(4096, n)
+    smp = (np.arange(S, dtype=np.int64) * n) // S
+    idx = max(0, int(np.ceil(q * S)) - 1)
+    bad = []
+    for u in sample:
+        t = np.sort(np.abs(rk[smp] - rk[u]).max(1))[idx]
+        gap = np.abs(rk - rk[u]).max(1)
+        within = np.flatnonzero(gap <= t)
+        within = within[within != u]
+        if not len(within):
+            continue
+        dd = ((x[within].astype(np.float64) - x[u].astype(np.float64)) ** 2).sum(1)
+        best = dd.min()
+        row = adj[u][adj[u] != 0xFFFFFFFF].astype(np.int64)
+        rd = ((x[row].astype(np.float64) - x[u].astype(np.float64)) ** 2).sum(1)
+        inrow = np.isin(row, within)
+        if not inrow.any() or rd[inrow].min() > best * (1 + 1e-5) + 1e-12:
+            bad.append(int(u))
+    return bad
+
+
 def _check_graph(x, adj, entry, R):
     from workloads import graph
     n = x.shape[0]
@@ -104,6 +140,7 @@ def test_tiny_built_in_library():
     _check_graph(d.vectors, adj, entry, wl.R)
     assert repaired >= 0
     assert not _nn_rows_ok(d.vectors, adj, np.arange(wl.n))
+    assert not _attr_level0_ok(d.attrs, types, d.vectors, adj, np.arange(0, wl.n, 7))
     for mode in ({}, {"fused": True}, {"split": True}):
         _parity(ix, d.vectors, d.attrs, types, d.queries, d.ranges, wl, adj, entry, **mode)
     ix.close()
@@ -123,9 +160,33 @@ def test_100k_built_in_library(name):
     sample = np.sort(np.random.default_rng(3).choice(wl.n, 1000, replace=False))
     bad = _nn_rows_ok(d.vectors, adj, sample)
     assert not bad, f"{len(bad)} sampled rows miss their nearest neighbour (first {bad[:5]})"
+    bad = _attr_level0_ok(d.attrs, types, d.vectors, adj, sample[:300])
+    assert not bad, f"{len(bad)} sampled rows miss their nearest attribute-close point (first {bad[:5]})"
     qs = np.sort(np.random.default_rng(4).choice(wl.nq, 200, replace=False))
     _parity(ix, d.vectors, d.attrs, types, d.queries, d.ranges, wl, adj, entry, sample=qs, split=True)
     ix.close()
+
+
+def test_vector_only_build_and_build_params():
+    """attr_levels = 0: the graph from vector distances only; alpha = 1
+    (the plain relative-neighbourhood rule) keeps fewer edges than 1.2."""
+    from workloads import gen
+    wl = gen.TINY
+    d = gen.generate(wl)
+    types = np.array(wl.attr_dtypes, dtype=np.int32)
+    boa = _boa()
+    edges = {}
+    for alpha in (1.0, 1.2):
+        ix = boa.Index(d.vectors, d.attrs, types, None, -1, R=wl.R, alpha=alpha, attr_levels=0)
+        adj, entry, _ = ix.graph()
+        _check_graph(d.vectors, adj, entry, wl.R)
+        assert not _nn_rows_ok(d.vectors, adj, np.arange(0, wl.n, 5))
+        edges[alpha] = int((adj != 0xFFFFFFFF).sum())
+        _parity(ix, d.vectors, d.attrs, types, d.queries, d.ranges, wl, adj, entry, split=True)
+        ix.close()
+    assert edges[1.0] < edges[1.2]
+    with pytest.raises(boa.BoaError):
+        boa.Index(d.vectors, d.attrs, types, None, -1, R=wl.R, alpha=0.5)
 
 
 def test_single_point_and_tiny_n():
