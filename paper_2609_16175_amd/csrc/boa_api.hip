@@ -463,7 +463,8 @@ PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t m
     h = std::max<uint32_t>(h, min_table_slots(ix));
     pl.h_slots = (int32_t)h;
     const int32_t Lb = (L + 1) & ~1, pw = ((L >> 6) + 3) & ~1;
-    pl.lds_per_wave = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + 2 * (int32_t)h;
+    pl.lds_per_wave = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + scorer_lds_bytes(ix->vec_dtype, ix->view.d, wide) +
+                      2 * (int32_t)h;
     pl.lds_per_wave = (pl.lds_per_wave + 15) & ~15;
     // waves per block: the choice with the most resident waves per CU
     int best_w = 0, best_wpb = 1, best_occ = 1;
@@ -547,7 +548,8 @@ PhasePlan plan_bitmap(const boa_index *ix, int32_t L, int64_t S)
     pl.h_slots = 0;
     const int64_t words = ((ix->view.n + 31) / 32 + 3) & ~(int64_t)3;
     const int32_t Lb = (L + 1) & ~1, pw = ((L >> 6) + 3) & ~1;
-    const int64_t lds = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + 4 * words;
+    const int64_t lds = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + scorer_lds_bytes(ix->vec_dtype, ix->view.d, true) +
+                        4 * words;
     pl.lds_per_wave = (int32_t)((lds + 15) & ~(int64_t)15);
     pl.wpb = 1;
     if ((size_t)pl.lds_per_wave > ix->lds_per_block_hw) return pl;   // capacity 0: not possible

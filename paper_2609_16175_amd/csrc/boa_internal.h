@@ -109,6 +109,8 @@ hipError_t build_graph(const void *d_vectors, int64_t n, int32_t d, int vec_dtyp
 // hold few waves per CU)
 hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st, bool wide = false);
 int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds, bool wide = false);
+// per-wave LDS bytes the distance scorer keeps (its copy of the query)
+int scorer_lds_bytes(int vec_dtype, int d, bool wide = false);
 hipError_t launch_compact(const CompactArgs &a, hipStream_t st);
 hipError_t launch_append(const AppendArgs &a, hipStream_t st);
 hipError_t launch_init(const InitArgs &a, hipStream_t st);

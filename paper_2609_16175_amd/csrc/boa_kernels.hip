@@ -141,16 +141,35 @@ template <int T, int W = 1>
 struct F32Scorer {
     // lane p = lane & 15 accumulates float4 chunks p, p+16, p+32, ...
     static constexpr bool kWide = W == 2;
-    float4 q[T];
+    // rows of more than 320 dimensions keep the query in LDS rather than in
+    // 4T registers (every 16-lane group reads the same chunks: broadcasts)
+    static constexpr bool kQueryLds = T >= 6;
+    static constexpr int kLdsBytes = kQueryLds ? 16 * T * 16 : 0;
+    float4 q[kQueryLds ? 1 : T];
+    float4 *ql = nullptr;
+
+    __device__ __forceinline__ void bind_lds(void *buf) { ql = reinterpret_cast<float4 *>(buf); }
+
+    __device__ __forceinline__ float4 qchunk(int t, int p) const
+    {
+        if constexpr (kQueryLds) return ql[p + 16 * t];
+        else return q[t];
+    }
 
     __device__ __forceinline__ void load_query(const void *Q, uint32_t qi, int d, int lane)
     {
         const float4 *qq = reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(Q) + (size_t)qi * d);
         int p = lane & 15, nch = d >> 2;
+        if constexpr (kQueryLds) {
+            // chunks 0 .. 16T-1, zero past the row (the caller's wave_sync
+            // orders these writes before the reads)
+            for (int cc = lane; cc < 16 * T; cc += 64) ql[cc] = cc < nch ? qq[cc] : make_float4(0.f, 0.f, 0.f, 0.f);
+        } else {
 #pragma unroll
-        for (int t = 0; t < T; ++t) {
-            int cc = p + 16 * t;
-            q[t] = cc < nch ? qq[cc] : make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int t = 0; t < T; ++t) {
+                int cc = p + 16 * t;
+                q[t] = cc < nch ? qq[cc] : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
         }
     }
 
@@ -213,19 +232,18 @@ struct F32Scorer {
     // x[t]); lane 15 of the group returns it
     __device__ __forceinline__ float dist(float4 (&x)[T], int p, int nch) const
     {
-#pragma unroll
-        for (int t = 0; t < T; ++t)
-            if (p + 16 * t >= nch) x[t] = q[t];   // past the row end: adds zero
         float acc = 0.0f;
 #pragma unroll
         for (int t = 0; t < T; ++t) {
-            float a0 = x[t].x - q[t].x;
+            const float4 qv = qchunk(t, p);
+            if (p + 16 * t >= nch) x[t] = qv;   // past the row end: adds zero
+            float a0 = x[t].x - qv.x;
             acc = __builtin_fmaf(a0, a0, acc);
-            float a1 = x[t].y - q[t].y;
+            float a1 = x[t].y - qv.y;
             acc = __builtin_fmaf(a1, a1, acc);
-            float a2 = x[t].z - q[t].z;
+            float a2 = x[t].z - qv.z;
             acc = __builtin_fmaf(a2, a2, acc);
-            float a3 = x[t].w - q[t].w;
+            float a3 = x[t].w - qv.w;
             acc = __builtin_fmaf(a3, a3, acc);
         }
         // pairwise tree over the 16 partials (p += p+8, +4, +2, +1), mirrored
@@ -244,7 +262,10 @@ struct U8Scorer {
     // lane p = lane % G holds the query's 16-byte chunk p (p < d/16); the
     // exact int32 sum is order-free.
     static constexpr bool kWide = W == 2;
+    static constexpr int kLdsBytes = 0;
     uint4 q;
+
+    __device__ __forceinline__ void bind_lds(void *) {}
 
     __device__ __forceinline__ void load_query(const void *Q, uint32_t qi, int d, int lane)
     {
@@ -454,7 +475,8 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     uint64_t *posbm = nkey + 64;                                 // pw >= L/64 + 2
     uint32_t *cid = reinterpret_cast<uint32_t *>(posbm + pw);   // 64
     float *cd = reinterpret_cast<float *>(cid + 64);             // 64
-    uint32_t *htab = reinterpret_cast<uint32_t *>(cd + 64);      // H/2 words (H 16-bit slots)
+    unsigned char *qlds = reinterpret_cast<unsigned char *>(cd + 64);   // the scorer's query copy, if any
+    uint32_t *htab = reinterpret_cast<uint32_t *>(qlds + Scorer::kLdsBytes);   // H/2 words (H 16-bit slots)
 
     const IndexView ix = a.ix;
     const int R = ix.R, d = ix.d, m = ix.m;
@@ -474,6 +496,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     const uint32_t table_words = a.vis_bitmap ? a.vis_words : (1u << a.h_log2) >> 1;
 
     Scorer sc;
+    sc.bind_lds(qlds);
     // one point's attribute record (m_pad cells) and its violation count
     auto load_attrs = [&](uint32_t id, int4 &w0, int4 &w1) {
         const int32_t *ar = ix.attrs + (size_t)id * ix.m_pad;
@@ -943,6 +966,19 @@ hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream
     hipError_t e = hipSuccess;
     BOA_DISPATCH(vec_dtype, a.ix.d, wide, e = launch_phase_t<S_>(a, blocks, st));
     return e;
+}
+
+template <class Scorer>
+static int scorer_lds_t()
+{
+    return Scorer::kLdsBytes;
+}
+
+int scorer_lds_bytes(int vec_dtype, int d, bool wide)
+{
+    int r = 0;
+    BOA_DISPATCH(vec_dtype, d, wide, r = scorer_lds_t<S_>());
+    return r;
 }
 
 int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds, bool wide)
