@@ -37,7 +37,8 @@ class _Index(C.Structure):
     _fields_ = [("n", C.c_int64), ("d", C.c_int32), ("vec_dtype", C.c_int32),
                 ("vectors", C.c_void_p), ("m", C.c_int32), ("attrs", C.c_void_p),
                 ("attr_dtypes", C.c_void_p), ("R", C.c_int32), ("adj", C.c_void_p),
-                ("entry", C.c_int64)]
+                ("entry", C.c_int64), ("pq_m", C.c_int32), ("pq_cb", C.c_void_p),
+                ("pq_codes", C.c_void_p)]
 
 
 _lib = None
@@ -53,6 +54,10 @@ def lib():
         L.orc_dist_f32.argtypes = [P, P, C.c_int32]
         L.orc_dist_u8.restype = C.c_float
         L.orc_dist_u8.argtypes = [P, P, C.c_int32]
+        L.orc_pq_table.restype = None
+        L.orc_pq_table.argtypes = [C.POINTER(_Index), P, P]
+        L.orc_pq_dist.restype = C.c_float
+        L.orc_pq_dist.argtypes = [P, P, C.c_int32]
         L.orc_phi.restype = C.c_int32
         L.orc_phi.argtypes = [P, P, P, C.c_int32]
         L.orc_confident.restype = C.c_int
@@ -80,12 +85,17 @@ def _p(a: np.ndarray):
 
 @dataclass
 class Index:
-    """Host-side view of a graph index for the oracle (keeps arrays alive)."""
+    """Host-side view of a graph index for the oracle (keeps arrays alive).
+    pq_codebook (M x 16 x d/M float32) and pq_codes (n x M/2 uint8, see
+    workloads.pq): traverse with product-quantised distances and re-rank
+    the results exactly."""
     vectors: np.ndarray
     attrs: np.ndarray
     attr_dtypes: np.ndarray
     adj: np.ndarray
     entry: int
+    pq_codebook: np.ndarray = None
+    pq_codes: np.ndarray = None
 
     def __post_init__(self):
         self.vectors = np.ascontiguousarray(self.vectors)
@@ -97,10 +107,18 @@ class Index:
         assert d % 4 == 0
         assert self.attrs.shape == (n, self.attr_dtypes.shape[0])
         assert self.adj.shape[0] == n
+        pq_m, cb_p, codes_p = 0, None, None
+        if self.pq_codebook is not None:
+            self.pq_codebook = np.ascontiguousarray(self.pq_codebook, dtype=np.float32)
+            self.pq_codes = np.ascontiguousarray(self.pq_codes, dtype=np.uint8)
+            pq_m = self.pq_codebook.shape[0]
+            assert self.pq_codebook.shape == (pq_m, 16, d // pq_m) and d % pq_m == 0 and pq_m % 2 == 0
+            assert self.pq_codes.shape == (n, pq_m // 2)
+            cb_p, codes_p = _p(self.pq_codebook).value, _p(self.pq_codes).value
         self._c = _Index(n, d, 1 if self.vectors.dtype == np.uint8 else 0, _p(self.vectors).value,
                          self.attr_dtypes.shape[0], _p(self.attrs).value,
                          _p(self.attr_dtypes).value, self.adj.shape[1], _p(self.adj).value,
-                         int(self.entry))
+                         int(self.entry), pq_m, cb_p, codes_p)
 
     @property
     def n(self):
@@ -123,6 +141,21 @@ def dist(x: np.ndarray, q: np.ndarray) -> float:
     q = np.ascontiguousarray(q, dtype=x.dtype)
     f = lib().orc_dist_u8 if x.dtype == np.uint8 else lib().orc_dist_f32
     return float(f(_p(x), _p(q), x.shape[0]))
+
+
+def pq_table(ix: Index, q) -> np.ndarray:
+    """The query's PQ distance table (M x 16 float32)."""
+    qq = np.ascontiguousarray(q, dtype=ix.vectors.dtype)
+    t = np.zeros(ix.pq_codebook.shape[0] * 16, dtype=np.float32)
+    lib().orc_pq_table(C.byref(ix._c), _p(qq), _p(t))
+    return t.reshape(-1, 16)
+
+
+def pq_dist(table: np.ndarray, code: np.ndarray) -> float:
+    """Asymmetric distance of one packed code through a query's table."""
+    t = np.ascontiguousarray(table, dtype=np.float32)
+    c = np.ascontiguousarray(code, dtype=np.uint8)
+    return float(lib().orc_pq_dist(_p(t), _p(c), t.shape[0]))
 
 
 def phi(attr_row, range_row, attr_dtypes) -> int:

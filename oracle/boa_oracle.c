@@ -39,6 +39,12 @@ typedef struct {
     int32_t R;
     const uint32_t *adj;        /* n x R, ORC_PAD padded */
     int64_t entry;              /* entry point s */
+    /* product quantisation (pq_m = 0: none): pq_m subspaces of d / pq_m
+     * dimensions, 16 centroids each (pq_cb: pq_m x 16 x ds float32), codes
+     * n x pq_m / 2 bytes, subspace 2b in the low nibble of byte b */
+    int32_t pq_m;
+    const float *pq_cb;
+    const uint8_t *pq_codes;
 } orc_index;
 
 /* One worklist entry: the search orders by the filter distance phi first,
@@ -110,6 +116,45 @@ static float point_dist(const orc_index *ix, uint32_t v, const void *q)
 }
 
 /* ------------------------------------------------------------------------
+ * Product-quantised asymmetric distance (Alg. 2 "PQDist"; Sec. III-B: the
+ * GPU builds each query's distance table, then scores a candidate as the
+ * sum of table entries indexed by its codes).
+ *   table:    T[m][c] = squared distance of the query's subvector m to
+ *             centroid c of subspace m, float32, one fused multiply-add per
+ *             dimension in dimension order from +0;
+ *   distance: 16 partial sums, subspace m added (float32) to partial
+ *             m mod 16 in increasing m, then the partials summed pairwise
+ *             (p += p+8, +4, +2, +1), the order of the exact distance. */
+void orc_pq_table(const orc_index *ix, const void *q, float *table)
+{
+    const int32_t M = ix->pq_m, ds = ix->d / M;
+    for (int m = 0; m < M; ++m)
+        for (int c = 0; c < 16; ++c) {
+            float acc = 0.0f;
+            for (int j = 0; j < ds; ++j) {
+                float qv = ix->vec_dtype == ORC_VEC_U8 ? (float)((const uint8_t *)q)[m * ds + j]
+                                                       : ((const float *)q)[m * ds + j];
+                float diff = qv - ix->pq_cb[((int64_t)m * 16 + c) * ds + j];
+                acc = fmaf(diff, diff, acc);
+            }
+            table[m * 16 + c] = acc;
+        }
+}
+
+float orc_pq_dist(const float *table, const uint8_t *code, int32_t M)
+{
+    float acc[16];
+    for (int p = 0; p < 16; ++p) acc[p] = 0.0f;
+    for (int m = 0; m < M; ++m) {
+        int c = (code[m / 2] >> (4 * (m % 2))) & 15;
+        acc[m % 16] = acc[m % 16] + table[m * 16 + c];
+    }
+    for (int s = 8; s >= 1; s /= 2)
+        for (int p = 0; p < s; ++p) acc[p] = acc[p] + acc[p + s];
+    return acc[0];
+}
+
+/* ------------------------------------------------------------------------
  * Filter distance phi: the number of the query's range predicates the
  * point violates (Sec. II, JAG paragraph; Alg. 2). A predicate on
  * attribute j holds when lo_j <= a^j <= hi_j, bounds inclusive (Def. 2,
@@ -144,6 +189,7 @@ typedef struct {
     uint32_t cur;
     orc_entry *beam, *cand, *tmp;
     int64_t cap_beam;
+    float *table;       /* the current query's PQ distance table (PQ only) */
 } orc_ws;
 
 static int ws_init(orc_ws *w, const orc_index *ix, int32_t Lmax)
@@ -154,12 +200,13 @@ static int ws_init(orc_ws *w, const orc_index *ix, int32_t Lmax)
     w->beam = (orc_entry *)malloc(sizeof(orc_entry) * (size_t)(Lmax + ix->R + 1));
     w->cand = (orc_entry *)malloc(sizeof(orc_entry) * (size_t)(ix->R + 1));
     w->tmp = (orc_entry *)malloc(sizeof(orc_entry) * (size_t)(Lmax + ix->R + 1));
-    return w->stamp && w->beam && w->cand && w->tmp;
+    w->table = ix->pq_m > 0 ? (float *)malloc(sizeof(float) * 16 * (size_t)ix->pq_m) : NULL;
+    return w->stamp && w->beam && w->cand && w->tmp && (ix->pq_m == 0 || w->table);
 }
 
 static void ws_free(orc_ws *w)
 {
-    free(w->stamp); free(w->beam); free(w->cand); free(w->tmp);
+    free(w->stamp); free(w->beam); free(w->cand); free(w->tmp); free(w->table);
 }
 
 static void ws_new_search(orc_ws *w, int64_t n)
@@ -171,14 +218,42 @@ static void ws_new_search(orc_ws *w, int64_t n)
     }
 }
 
-static orc_entry score(const orc_index *ix, uint32_t v, const void *q, const int32_t *rr)
+/* A candidate's key. With product quantisation the traversal orders by the
+ * asymmetric distance through the query's table (Alg. 2 "PQDist"). */
+static orc_entry score(const orc_index *ix, uint32_t v, const void *q, const int32_t *rr, const float *table)
 {
     orc_entry e;
     e.phi = orc_phi(ix->attrs + (int64_t)v * ix->m, rr, ix->attr_dtypes, ix->m);
-    e.d = point_dist(ix, v, q);
+    e.d = table ? orc_pq_dist(table, ix->pq_codes + (int64_t)v * (ix->pq_m / 2), ix->pq_m)
+                : point_dist(ix, v, q);
     e.id = v;
     e.expanded = 0;
     return e;
+}
+
+/* The result of a search (the first L entries of its sorted list): the
+ * filter-valid entries, in order. With product quantisation they are
+ * re-ranked by exact distance (Sec. III-B step 8: on convergence the
+ * accumulated candidates are ranked by exact distance under a hard
+ * predicate), ordered by (exact distance, id). Returns n_valid; out holds
+ * the valid entries with their reported distances. */
+static int valid_results(const orc_index *ix, const orc_entry *beam, int lim, const void *q, orc_entry *out)
+{
+    int n_valid = 0;
+    while (n_valid < lim && beam[n_valid].phi == 0) {
+        out[n_valid] = beam[n_valid];
+        ++n_valid;
+    }
+    if (ix->pq_m > 0) {
+        for (int a = 0; a < n_valid; ++a) out[a].d = point_dist(ix, out[a].id, q);
+        for (int a = 1; a < n_valid; ++a) {   /* insertion sort by (d, id) */
+            orc_entry x = out[a];
+            int b = a - 1;
+            while (b >= 0 && entry_before(&x, &out[b])) { out[b + 1] = out[b]; --b; }
+            out[b + 1] = x;
+        }
+    }
+    return n_valid;
 }
 
 /* ------------------------------------------------------------------------
@@ -204,8 +279,9 @@ static int search_one(const orc_index *ix, orc_ws *w, const void *q, const int32
 {
     orc_entry *beam = w->beam, *cand = w->cand, *tmp = w->tmp;
     ws_new_search(w, ix->n);
+    if (w->table) orc_pq_table(ix, q, w->table);
     int len = 1;
-    beam[0] = score(ix, (uint32_t)ix->entry, q, rr);
+    beam[0] = score(ix, (uint32_t)ix->entry, q, rr, w->table);
     w->stamp[ix->entry] = w->cur;
     *S += 1;
 
@@ -223,7 +299,7 @@ static int search_one(const orc_index *ix, orc_ws *w, const void *q, const int32
             if (v == ORC_PAD) continue;
             if (w->stamp[v] == w->cur) continue;
             w->stamp[v] = w->cur;
-            cand[c++] = score(ix, v, q, rr);
+            cand[c++] = score(ix, v, q, rr, w->table);
         }
         *S += c;
 
@@ -326,14 +402,14 @@ static void run_query(phase_job *J, orc_ws *w, int64_t t)
     int64_t E = 0, S = 0;
     search_one(ix, w, q, rr, J->L, &len, &E, &S);
 
-    int n_valid = 0;
-    while (n_valid < len && w->beam[n_valid].phi == 0) ++n_valid;
+    orc_entry *res = (orc_entry *)malloc(sizeof(orc_entry) * (size_t)(len > 0 ? len : 1));
+    int n_valid = valid_results(ix, w->beam, len, q, res);
     float *vd = (float *)malloc(sizeof(float) * (size_t)(n_valid > 0 ? n_valid : 1));
-    for (int a = 0; a < n_valid; ++a) vd[a] = w->beam[a].d;
+    for (int a = 0; a < n_valid; ++a) vd[a] = res[a].d;
     for (int a = 0; a < J->k; ++a) {
         if (a < n_valid) {
-            J->ids[i * J->k + a] = w->beam[a].id;
-            J->dists[i * J->k + a] = w->beam[a].d;
+            J->ids[i * J->k + a] = res[a].id;
+            J->dists[i * J->k + a] = res[a].d;
         } else {
             J->ids[i * J->k + a] = ORC_PAD;
             J->dists[i * J->k + a] = INFINITY;
@@ -342,6 +418,7 @@ static void run_query(phase_job *J, orc_ws *w, int64_t t)
     J->final_L[i] = J->L;
     J->conf[t] = (uint8_t)orc_confident(vd, n_valid, J->k, J->eps);
     free(vd);
+    free(res);
     if (J->q_E) J->q_E[i] += E;
     if (J->q_S) J->q_S[i] += S;
 }
@@ -535,7 +612,7 @@ static void search_continue(const orc_index *ix, orc_ws *w, const void *q, const
             if (v == ORC_PAD) continue;
             if (w->stamp[v] == w->cur) continue;
             w->stamp[v] = w->cur;
-            cand[c++] = score(ix, v, q, rr);
+            cand[c++] = score(ix, v, q, rr, w->table);
         }
         *S += c;
 
@@ -568,7 +645,8 @@ int32_t orc_boa_warm(const orc_index *ix, const void *queries, const int32_t *ra
     orc_ws w;
     if (!ws_init(&w, ix, Lmax)) return -2;
     float *vd = (float *)malloc(sizeof(float) * (size_t)Lmax);
-    if (!vd) { ws_free(&w); return -2; }
+    orc_entry *res = (orc_entry *)malloc(sizeof(orc_entry) * (size_t)Lmax);
+    if (!vd || !res) { free(vd); free(res); ws_free(&w); return -2; }
     size_t qbytes = (size_t)ix->d * (ix->vec_dtype == ORC_VEC_U8 ? 1 : 4);
     if (phase_stats) memset(phase_stats, 0, sizeof(int64_t) * 5 * (size_t)n_phases);
     int32_t ran = 0;
@@ -578,8 +656,9 @@ int32_t orc_boa_warm(const orc_index *ix, const void *queries, const int32_t *ra
         int64_t Et = 0, St = 0;
         /* the entry point, scored and marked before the first expansion */
         ws_new_search(&w, ix->n);
+        if (w.table) orc_pq_table(ix, q, w.table);
         int len = 1;
-        w.beam[0] = score(ix, (uint32_t)ix->entry, q, rr);
+        w.beam[0] = score(ix, (uint32_t)ix->entry, q, rr, w.table);
         w.stamp[ix->entry] = w.cur;
         int64_t S0 = 1;
         for (int p = 0; p < n_phases; ++p) {
@@ -589,11 +668,11 @@ int32_t orc_boa_warm(const orc_index *ix, const void *queries, const int32_t *ra
             S0 = 0;
             search_continue(ix, &w, q, rr, L, cap, &len, &E, &S);
             int lim = len < L ? len : L;
-            int n_valid = 0;
-            while (n_valid < lim && w.beam[n_valid].phi == 0) { vd[n_valid] = w.beam[n_valid].d; ++n_valid; }
+            int n_valid = valid_results(ix, w.beam, lim, q, res);
+            for (int a = 0; a < n_valid; ++a) vd[a] = res[a].d;
             for (int a = 0; a < k; ++a) {
-                ids[i * k + a] = a < n_valid ? w.beam[a].id : ORC_PAD;
-                dists[i * k + a] = a < n_valid ? w.beam[a].d : INFINITY;
+                ids[i * k + a] = a < n_valid ? res[a].id : ORC_PAD;
+                dists[i * k + a] = a < n_valid ? res[a].d : INFINITY;
             }
             final_L[i] = L;
             Et += E;
@@ -613,6 +692,7 @@ int32_t orc_boa_warm(const orc_index *ix, const void *queries, const int32_t *ra
         if (q_S) q_S[i] = St;
     }
     free(vd);
+    free(res);
     ws_free(&w);
     return ran;
 }
