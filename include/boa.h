@@ -163,6 +163,11 @@ typedef struct {
                                The first phase is unchanged; later phases differ from a
                                restart. Runs in the fused mode only (fused = 1, so
                                tau == 0), else BOA_EUNSUPPORTED. 0: every phase restarts. */
+    int32_t pq;             /* 1: traverse with product-quantised distances (Alg. 2 "PQDist",
+                               the index needs boa_set_pq), then at each phase's end
+                               re-rank the phase's valid worklist entries by exact
+                               distance (Sec. III-B step 8); the result and Eq. 3 read
+                               the re-ranked entries. k <= 128. 0: exact distances. */
 } boa_params;
 
 void boa_default_params(boa_params *p);
@@ -250,6 +255,21 @@ int boa_get_stats(const boa_index *idx, boa_stats *out);
 
 /* Zero the accumulated counters of boa_stats. */
 int boa_reset_counters(boa_index *idx);
+
+/*
+ * Product-quantisation data of an index (Alg. 2 "PQDist"; Sec. III-B), copied
+ * to the device (the caller may free its arrays on return).
+ *   codebook  HOST, M x 16 x (d / M) float32: 16 centroids per subspace of
+ *             d / M consecutive dimensions.
+ *   codes     HOST, n x M / 2 bytes: byte b holds the centroid of subspace 2b
+ *             in its low nibble and of subspace 2b + 1 in its high nibble.
+ *   M         even, <= 256, dividing d.
+ * The per-query distance table entry (m, c) is the float32 fused
+ * multiply-add chain over the subspace's dimensions of (q - centroid)^2; the
+ * asymmetric distance adds a point's table entries in 16 partial sums
+ * (subspace m into partial m mod 16, increasing m) summed pairwise.
+ * Errors: BOA_EINVAL, BOA_ENOMEM, BOA_EHIP. */
+int boa_set_pq(boa_index *idx, const float *codebook, const uint8_t *codes, int32_t M);
 
 /* The graph and entry point an index searches (e.g. the ones the library
  * built). adjacency: HOST n x R uint32, or NULL; entry: the entry point s,

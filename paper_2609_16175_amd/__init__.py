@@ -39,7 +39,7 @@ class Params(C.Structure):
                 ("eps", C.c_double), ("tau", C.c_double), ("fixed_L", C.c_int32),
                 ("boa_plus", C.c_int32), ("sub_batches", C.c_int32), ("lds_hash_slots", C.c_int32),
                 ("schedule", C.POINTER(C.c_int32)), ("n_schedule", C.c_int32), ("fused", C.c_int32),
-                ("warm_start", C.c_int32)]
+                ("warm_start", C.c_int32), ("pq", C.c_int32)]
 
 
 class BuildParams(C.Structure):
@@ -88,6 +88,8 @@ def lib():
                                          P, C.c_int32, C.c_int64, C.POINTER(BuildParams), C.POINTER(P)]
         L.boa_default_build_params.restype = None
         L.boa_default_build_params.argtypes = [C.POINTER(BuildParams)]
+        L.boa_set_pq.restype = C.c_int
+        L.boa_set_pq.argtypes = [P, P, P, C.c_int32]
         L.boa_get_graph.restype = C.c_int
         L.boa_get_graph.argtypes = [P, P, C.POINTER(C.c_int64), C.POINTER(C.c_int64)]
         L.boa_free_index.restype = None
@@ -158,6 +160,16 @@ class Index:
         self.n, self.d, self.m, self.R = n, d, types.shape[0], width
         self.vec_dtype = vt
 
+    def set_pq(self, codebook: np.ndarray, codes: np.ndarray):
+        """Product-quantisation data: codebook M x 16 x d/M float32, codes
+        n x M/2 uint8 (workloads.pq layout)."""
+        cb = np.ascontiguousarray(codebook, dtype=np.float32)
+        cc = np.ascontiguousarray(codes, dtype=np.uint8)
+        M = cb.shape[0]
+        if cb.shape != (M, 16, self.d // M) or cc.shape != (self.n, M // 2):
+            raise ValueError("codebook must be M x 16 x d/M and codes n x M/2")
+        _check(lib().boa_set_pq(self._h, cb.ctypes.data, cc.ctypes.data, M))
+
     def graph(self):
         """(adjacency n x R uint32, entry, repaired): the graph the index
         searches; repaired counts the in-edges the library's construction
@@ -182,7 +194,8 @@ class Index:
                eps: float = 0.05, tau: float = 0.0, fixed_L: int = 0, boa_plus: bool = False,
                sub_batches: int = 10, lds_hash_slots: int = 0, schedule=None, fused: bool = False,
                split: bool = False, counters: bool = False,
-               stream=None, out=None, no_alloc: bool = False, warm: bool = False) -> SearchResult:
+               stream=None, out=None, no_alloc: bool = False, warm: bool = False,
+               pq: bool = False) -> SearchResult:
         """Adaptive filtered top-k of a batch of device-resident queries.
 
         queries: torch tensor (nq, d) on the GPU, float32 or uint8 like the index.
@@ -191,6 +204,8 @@ class Index:
                  one launch, the survivors through all later phases in a second.
         warm:    warm-start escalation (fused mode): each phase continues from
                  the previous phase's list and visited set.
+        pq:      traverse with product-quantised distances (set_pq first) and
+                 re-rank each phase's valid entries exactly.
         no_alloc: call boa_search_noalloc (the library allocates no device
                  memory for the call; pass preallocated `out` tensors to
                  allocate nothing on the torch side either).
@@ -222,6 +237,7 @@ class Index:
             raise ValueError("fused and split are exclusive")
         p.fused = 2 if split else int(fused)
         p.warm_start = int(warm)
+        p.pq = int(pq)
         sched_arr = None
         if schedule is not None:
             sched_arr = (C.c_int32 * len(schedule))(*schedule)

@@ -101,6 +101,9 @@ struct boa_index {
     int32_t *d_attrs = nullptr;
     uint32_t *d_adj = nullptr;
 
+    float *d_pq_cb = nullptr;        // product quantisation (boa_set_pq)
+    uint8_t *d_pq_codes = nullptr;
+    int32_t pq_m = 0;
     bool built_graph = false;        // the graph was constructed by the library
     BuildStats build_stats{};
 
@@ -125,6 +128,7 @@ struct boa_index {
     // last search
     int64_t last_nq = 0;
     int32_t last_k = 0;
+    int32_t last_pq_m = 0;
     std::vector<PhasePlan> plans;
     std::vector<std::pair<int, int>> launch_phase;  // (phase, event index)
     hipEvent_t ev_all0 = nullptr, ev_all1 = nullptr;
@@ -168,6 +172,8 @@ void boa_free_index(boa_index *ix)
     dfree(ix->d_vectors);
     dfree(ix->d_attrs);
     dfree(ix->d_adj);
+    dfree(ix->d_pq_cb);
+    dfree(ix->d_pq_codes);
     dfree(ix->active[0]);
     dfree(ix->active[1]);
     dfree(ix->n_active);
@@ -449,7 +455,8 @@ uint32_t min_table_slots(const boa_index *ix)
     return std::max<uint32_t>(64u, B > 14 ? (8u << (B - 14)) : 64u);
 }
 
-PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t max_active, bool wide = false)
+PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t max_active, bool wide = false,
+                     int pq_m = 0)
 {
     PhasePlan pl{};
     pl.L = L;
@@ -463,14 +470,15 @@ PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t m
     h = std::max<uint32_t>(h, min_table_slots(ix));
     pl.h_slots = (int32_t)h;
     const int32_t Lb = (L + 1) & ~1, pw = ((L >> 6) + 3) & ~1;
-    pl.lds_per_wave = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + scorer_lds_bytes(ix->vec_dtype, ix->view.d, wide) +
-                      2 * (int32_t)h;
+    // (a product-quantised search also keeps its re-rank keys, Lb of them)
+    pl.lds_per_wave = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 +
+                      scorer_lds_bytes(ix->vec_dtype, ix->view.d, wide, pq_m) + (pq_m ? 8 * Lb : 0) + 2 * (int32_t)h;
     pl.lds_per_wave = (pl.lds_per_wave + 15) & ~15;
     // waves per block: the choice with the most resident waves per CU
     int best_w = 0, best_wpb = 1, best_occ = 1;
     for (int wpb = 4; wpb >= 1; wpb >>= 1) {
         if ((size_t)wpb * pl.lds_per_wave > ix->lds_per_block_max) continue;
-        int occ = phase_occupancy(ix->vec_dtype, ix->view.d, wpb, (size_t)wpb * pl.lds_per_wave, wide);
+        int occ = phase_occupancy(ix->vec_dtype, ix->view.d, wpb, (size_t)wpb * pl.lds_per_wave, wide, pq_m);
         if (occ * wpb > best_w) {
             best_w = occ * wpb;
             best_wpb = wpb;
@@ -519,12 +527,13 @@ int stage_profile_end(unsigned long long *prof, size_t pn, int L, int waves, hip
 // A phase's launch: the automatic table of plan_phase, then doubled (up to
 // 16384 slots) while that keeps as many waves resident (registers, not LDS,
 // often bound narrow phases, so a wider table and fewer spills come free).
-PhasePlan plan_phase_widest(const boa_index *ix, int32_t L, int32_t forced_h, int64_t max_active, bool wide = false)
+PhasePlan plan_phase_widest(const boa_index *ix, int32_t L, int32_t forced_h, int64_t max_active, bool wide = false,
+                            int pq_m = 0)
 {
-    PhasePlan best = plan_phase(ix, L, forced_h, max_active, wide);
+    PhasePlan best = plan_phase(ix, L, forced_h, max_active, wide, pq_m);
     if (forced_h > 0) return best;
     for (uint32_t h = 2u * (uint32_t)best.h_slots; h <= 16384u; h <<= 1) {
-        PhasePlan pl = plan_phase(ix, L, (int32_t)h, max_active, wide);
+        PhasePlan pl = plan_phase(ix, L, (int32_t)h, max_active, wide, pq_m);
         if ((size_t)pl.lds_per_wave > ix->lds_per_block_max || pl.capacity < best.capacity) break;
         best = pl;
     }
@@ -539,7 +548,7 @@ PhasePlan plan_phase_widest(const boa_index *ix, int32_t L, int32_t forced_h, in
 // wave per block): an exact set tested by a single LDS atomic, for indexes
 // small enough (n/8 bytes plus the worklist within the device's per-block
 // LDS) and survivor counts that it still lets be resident at once.
-PhasePlan plan_bitmap(const boa_index *ix, int32_t L, int64_t S)
+PhasePlan plan_bitmap(const boa_index *ix, int32_t L, int64_t S, int pq_m = 0)
 {
     PhasePlan pl{};
     pl.L = L;
@@ -548,28 +557,28 @@ PhasePlan plan_bitmap(const boa_index *ix, int32_t L, int64_t S)
     pl.h_slots = 0;
     const int64_t words = ((ix->view.n + 31) / 32 + 3) & ~(int64_t)3;
     const int32_t Lb = (L + 1) & ~1, pw = ((L >> 6) + 3) & ~1;
-    const int64_t lds = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + scorer_lds_bytes(ix->vec_dtype, ix->view.d, true) +
-                        4 * words;
+    const int64_t lds = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + scorer_lds_bytes(ix->vec_dtype, ix->view.d, true, pq_m) +
+                        (pq_m ? 8 * Lb : 0) + 4 * words;
     pl.lds_per_wave = (int32_t)((lds + 15) & ~(int64_t)15);
     pl.wpb = 1;
     if ((size_t)pl.lds_per_wave > ix->lds_per_block_hw) return pl;   // capacity 0: not possible
-    const int occ = phase_occupancy(ix->vec_dtype, ix->view.d, 1, (size_t)pl.lds_per_wave, true);
+    const int occ = phase_occupancy(ix->vec_dtype, ix->view.d, 1, (size_t)pl.lds_per_wave, true, pq_m);
     const int64_t blocks = (int64_t)std::max(occ, 0) * ix->num_cu;
     pl.capacity = blocks;
     pl.blocks = (int32_t)std::min<int64_t>(blocks, std::max<int64_t>(S, 1));
     return pl;
 }
 
-PhasePlan plan_escalation(const boa_index *ix, int32_t L, int64_t S, int32_t forced_h)
+PhasePlan plan_escalation(const boa_index *ix, int32_t L, int64_t S, int32_t forced_h, int pq_m = 0)
 {
-    if (forced_h > 0) return plan_phase(ix, L, forced_h, S, true);
+    if (forced_h > 0) return plan_phase(ix, L, forced_h, S, true, pq_m);
     {
-        PhasePlan bm = plan_bitmap(ix, L, S);
+        PhasePlan bm = plan_bitmap(ix, L, S, pq_m);
         if (bm.capacity >= S) return bm;
     }
-    PhasePlan dflt = plan_phase(ix, L, 0, S, true);
+    PhasePlan dflt = plan_phase(ix, L, 0, S, true, pq_m);
     for (uint32_t h = 16384; h > (uint32_t)dflt.h_slots; h >>= 1) {
-        PhasePlan pl = plan_phase(ix, L, (int32_t)h, S, true);
+        PhasePlan pl = plan_phase(ix, L, (int32_t)h, S, true, pq_m);
         if (pl.capacity >= S && (size_t)pl.lds_per_wave <= ix->lds_per_block_max) return pl;
     }
     return dflt;
@@ -598,6 +607,7 @@ struct Request {
     int32_t sched[BOA_MAX_PHASES];
     int32_t n_phases;
     bool plus, split, fused, warm;
+    int32_t pq_m;             // > 0: product-quantised traversal with that many subspaces
     int32_t sub;              // BOA+ sub-batches (1 otherwise)
     int32_t n_counters;
     uint32_t tau_count;
@@ -636,6 +646,10 @@ int validate(const boa_index *ix, const void *queries, const int32_t *ranges, in
     if (p->warm_start && !rq.fused)
         return fail(BOA_EUNSUPPORTED, "warm-start escalation runs in the fused mode (fused = 1)");
     rq.warm = p->warm_start == 1;
+    if (p->pq != 0 && p->pq != 1) return fail(BOA_EINVAL, "pq must be 0 or 1");
+    if (p->pq && ix->pq_m == 0) return fail(BOA_EINVAL, "pq = 1 needs product-quantisation codes (boa_set_pq)");
+    if (p->pq && p->k > 128) return fail(BOA_EUNSUPPORTED, "a product-quantised search returns at most k = 128");
+    rq.pq_m = p->pq ? ix->pq_m : 0;
     rq.sub = rq.plus ? std::min<int64_t>(p->sub_batches, std::max<int64_t>(nq, 1)) : 1;
     rq.n_counters = rq.n_phases * (rq.sub + 1) + 8;
     rq.tau_count = (uint32_t)std::floor(p->tau * (double)nq);
@@ -652,7 +666,7 @@ int plan_search(const boa_index *ix, const Request &rq, int64_t nq, int32_t forc
     for (int32_t ph = 0; ph < rq.n_phases; ++ph) {
         // a fused launch, and a BOA+ escalation launch, size LDS for the widest phase
         const bool wide = rq.fused || (rq.plus && ph > 0);
-        PhasePlan pl = plan_phase_widest(ix, wide ? Lw : rq.sched[ph], forced_h, nq);
+        PhasePlan pl = plan_phase_widest(ix, wide ? Lw : rq.sched[ph], forced_h, nq, false, rq.pq_m);
         pl.L = rq.sched[ph];
         if ((size_t)pl.lds_per_wave > ix->lds_per_block_max)
             return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
@@ -661,11 +675,11 @@ int plan_search(const boa_index *ix, const Request &rq, int64_t nq, int32_t forc
     }
     if (rq.split && rq.n_phases > 1) {
         // every grid the escalation launch may take (it has at most nq waves)
-        const PhasePlan d = plan_phase(ix, Lw, forced_h, nq, true);
+        const PhasePlan d = plan_phase(ix, Lw, forced_h, nq, true, rq.pq_m);
         slots = std::max<uint64_t>(slots, (uint64_t)d.blocks * d.wpb);
         if (forced_h <= 0)
             for (uint32_t h = 16384; h > (uint32_t)d.h_slots; h >>= 1) {
-                const PhasePlan c = plan_phase(ix, Lw, (int32_t)h, nq, true);
+                const PhasePlan c = plan_phase(ix, Lw, (int32_t)h, nq, true, rq.pq_m);
                 slots = std::max<uint64_t>(slots, (uint64_t)c.blocks * c.wpb);
             }
     }
@@ -734,6 +748,11 @@ int run_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_
     base.qstat = ws.qstat;
     base.qE = ws.qE;
     base.qS = ws.qS;
+    base.pq = rq.pq_m > 0 ? 1 : 0;
+    base.pq_m = rq.pq_m;
+    base.pq_cb = ix->d_pq_cb;
+    base.pq_codes = ix->d_pq_codes;
+    base.vec_u8 = ix->vec_dtype == BOA_VEC_U8 ? 1 : 0;
     for (int32_t ph = 0; ph < n_phases; ++ph) base.sched[ph] = sched[ph];
     int ev = 0;
     // one search launch, bracketed by HIP events when timing
@@ -799,7 +818,7 @@ int run_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_
             HIP_TRY(hipMemcpyAsync(&S, ws.n_active + 1, sizeof(S), hipMemcpyDeviceToHost, st));
             HIP_TRY(hipStreamSynchronize(st));
             if (S > 0) {
-                PhasePlan pe = plan_escalation(ix, Lw, S, p->lds_hash_slots);
+                PhasePlan pe = plan_escalation(ix, Lw, S, p->lds_hash_slots, rq.pq_m);
                 if ((size_t)pe.lds_per_wave > (pe.vis_bitmap ? ix->lds_per_block_hw : ix->lds_per_block_max))
                     return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
                 if (int rc = cap_to_slots(pe, ws.slots)) return rc;
@@ -976,6 +995,7 @@ int run_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_
         ix->plans.assign(plans, plans + n_phases);
         ix->last_nq = nq;
         ix->last_k = p->k;
+        ix->last_pq_m = rq.pq_m;
         ix->have_stats = true;
         ix->cum_searches += 1;
         for (auto &lp : ix->launch_phase) {
@@ -1129,7 +1149,10 @@ extern "C" int boa_get_stats(const boa_index *ix, boa_stats *out)
             ps.expansions += E[(size_t)ph * nq + i];
             ps.scored += S[(size_t)ph * nq + i];
         }
-        ps.gathered_bytes = 4.0 * v.R * (double)ps.expansions + (4.0 * v.m + v.d * e) * (double)ps.scored +
+        // a product-quantised search reads a point's code instead of its
+        // vector (the exact re-rank's reads are not counted here)
+        const double per_scored = ix->last_pq_m ? 4.0 * v.m + ix->last_pq_m / 2 : 4.0 * v.m + v.d * e;
+        ps.gathered_bytes = 4.0 * v.R * (double)ps.expansions + per_scored * (double)ps.scored +
                             (v.d * e + 8.0 * v.m + 8.0 * ix->last_k + 4.0) * (double)ps.active;
     }
     for (auto &lp : ix->launch_phase) {
@@ -1174,5 +1197,36 @@ extern "C" int boa_get_graph(const boa_index *ix, uint32_t *adjacency, int64_t *
         if (cur != ix->device) return fail(BOA_EINVAL, "index lives on another device than the current one");
         HIP_TRY(hipMemcpy(adjacency, ix->d_adj, (size_t)ix->view.n * ix->view.R * 4, hipMemcpyDeviceToHost));
     }
+    return BOA_OK;
+}
+
+extern "C" int boa_set_pq(boa_index *ix, const float *codebook, const uint8_t *codes, int32_t M)
+{
+    if (!ix || !codebook || !codes) return fail(BOA_EINVAL, "NULL argument");
+    const int32_t d = ix->view.d;
+    if (M < 2 || M % 2 || M > 256 || d % M) return fail(BOA_EINVAL, "M must be even, <= 256 and divide d");
+    const int64_t n = ix->view.n;
+    int cur = 0;
+    HIP_TRY(hipGetDevice(&cur));
+    if (cur != ix->device) return fail(BOA_EINVAL, "index lives on another device than the current one");
+    float *cb = nullptr;
+    uint8_t *cc = nullptr;
+    int rc;
+    if ((rc = dalloc(&cb, (size_t)M * 16 * (d / M)))) return rc;
+    if ((rc = dalloc(&cc, (size_t)n * (M / 2)))) {
+        dfree(cb);
+        return rc;
+    }
+    if (hipMemcpy(cb, codebook, (size_t)M * 16 * (d / M) * 4, hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(cc, codes, (size_t)n * (M / 2), hipMemcpyHostToDevice) != hipSuccess) {
+        dfree(cb);
+        dfree(cc);
+        return fail(BOA_EHIP, "upload of the product-quantisation data failed");
+    }
+    dfree(ix->d_pq_cb);
+    dfree(ix->d_pq_codes);
+    ix->d_pq_cb = cb;
+    ix->d_pq_codes = cc;
+    ix->pq_m = M;
     return BOA_OK;
 }

@@ -50,6 +50,11 @@ struct PhaseArgs {
     int32_t p_begin, p_end;   // phases run by this launch (one, or all when fused)
     int32_t write_conf;       // record each query's confidence for a compaction/append
     int32_t warm;             // warm-start escalation: phases continue from the previous one's state
+    int32_t pq;               // traverse with product-quantised distances, re-rank exactly
+    int32_t pq_m;             // subspaces (16 centroids each)
+    const float *pq_cb;       // pq_m x 16 x d/pq_m
+    const uint8_t *pq_codes;  // n x pq_m/2, subspace 2b in the low nibble of byte b
+    int32_t vec_u8;           // the vectors are uint8 (the exact re-rank's arithmetic)
     int32_t L_alloc;          // widest of them: sizes the per-wave LDS
     int32_t h_log2;           // log2 of the LDS visited-table slots (16-bit entries)
     int32_t vis_bitmap;       // 1: the visited set is instead an LDS bitmap over all n ids
@@ -108,9 +113,11 @@ hipError_t build_graph(const void *d_vectors, int64_t n, int32_t d, int vec_dtyp
 // wide: the scorer variant with twice the rows in flight (for launches that
 // hold few waves per CU)
 hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st, bool wide = false);
-int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds, bool wide = false);
-// per-wave LDS bytes the distance scorer keeps (its copy of the query)
-int scorer_lds_bytes(int vec_dtype, int d, bool wide = false);
+// pq_m > 0: the product-quantised scorer with that many subspaces
+int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds, bool wide = false, int pq_m = 0);
+// per-wave LDS bytes the distance scorer keeps (its copy of the query, or
+// the product-quantisation distance table)
+int scorer_lds_bytes(int vec_dtype, int d, bool wide = false, int pq_m = 0);
 hipError_t launch_compact(const CompactArgs &a, hipStream_t st);
 hipError_t launch_append(const AppendArgs &a, hipStream_t st);
 hipError_t launch_init(const InitArgs &a, hipStream_t st);

@@ -145,6 +145,7 @@ struct F32Scorer {
     // 4T registers (every 16-lane group reads the same chunks: broadcasts)
     static constexpr bool kQueryLds = T >= 6;
     static constexpr int kLdsBytes = kQueryLds ? 16 * T * 16 : 0;
+    static constexpr bool kPQ = false;
     float4 q[kQueryLds ? 1 : T];
     float4 *ql = nullptr;
 
@@ -263,6 +264,7 @@ struct U8Scorer {
     // exact int32 sum is order-free.
     static constexpr bool kWide = W == 2;
     static constexpr int kLdsBytes = 0;
+    static constexpr bool kPQ = false;
     uint4 q;
 
     __device__ __forceinline__ void bind_lds(void *) {}
@@ -344,6 +346,168 @@ struct U8Scorer {
         return acc;
     }
 };
+
+// Product-quantised asymmetric distance (Alg. 2 "PQDist"): 4-bit codes, 16
+// centroids per subspace. The query's distance table (M x 16 float32) lives
+// in LDS; a 16-lane group scores one candidate, lane p adding the entries of
+// subspaces p, p+16, ... in increasing order (nibble (p + 16t) of the packed
+// code), then the same pairwise tree as the exact float32 distance.
+template <int T>
+struct PQScorer {
+    static constexpr bool kWide = false;
+    static constexpr bool kPQ = true;
+    static constexpr int kLdsBytes = 16 * T * 16 * 4;   // the table of up to 16 T subspaces
+    float *lut = nullptr;
+    const uint8_t *codes = nullptr;
+    const float *cb = nullptr;
+    int M = 0, half = 0, ds = 0, u8 = 0;
+
+    __device__ __forceinline__ void bind_lds(void *buf) { lut = reinterpret_cast<float *>(buf); }
+    __device__ __forceinline__ void bind_pq(const uint8_t *c, int m, const float *codebook, int d, int vec_u8)
+    {
+        codes = c;
+        M = m;
+        half = m >> 1;
+        cb = codebook;
+        ds = d / m;
+        u8 = vec_u8;
+    }
+
+    // table entry (m, c): fma chain over the subspace's dimensions from +0
+    // (the caller's wave_sync orders these writes before the reads)
+    __device__ __forceinline__ void load_query(const void *Q, uint32_t qi, int d, int lane)
+    {
+        for (int e = lane; e < M * 16; e += 64) {
+            const int m = e >> 4, c = e & 15;
+            float acc = 0.0f;
+            for (int j = 0; j < ds; ++j) {
+                const size_t qo = (size_t)qi * d + m * ds + j;
+                const float qv = u8 ? (float)reinterpret_cast<const uint8_t *>(Q)[qo]
+                                    : reinterpret_cast<const float *>(Q)[qo];
+                const float diff = qv - cb[((size_t)m * 16 + c) * ds + j];
+                acc = __builtin_fmaf(diff, diff, acc);
+            }
+            lut[e] = acc;
+        }
+    }
+
+    static constexpr int RU = T <= 4 ? 4 : 2;   // rounds of 4 candidates per round trip
+    struct Ids {
+        uint32_t v[RU];
+    };
+
+    __device__ __forceinline__ void read_ids(const uint32_t *cid, int c, int r0, int lane, Ids &ids) const
+    {
+        const int g = lane >> 4;
+#pragma unroll
+        for (int u = 0; u < RU; ++u) {
+            const int cj = r0 + 4 * u + g;
+            ids.v[u] = cid[cj < c ? cj : 0];
+        }
+    }
+
+    __device__ __forceinline__ void score(const void *, int, const uint32_t *cid, int c, float *cd, int lane,
+                                          const Ids &first)
+    {
+        const int g = lane >> 4, p = lane & 15;
+        for (int r0 = 0; r0 < c; r0 += 4 * RU) {
+            Ids ids = first;
+            if (r0 > 0) read_ids(cid, c, r0, lane, ids);
+            uint32_t b[RU][T];
+#pragma unroll
+            for (int u = 0; u < RU; ++u) {
+                if (r0 + 4 * u < c) {   // uniform
+                    const uint8_t *row = codes + (size_t)ids.v[u] * half;
+#pragma unroll
+                    for (int t = 0; t < T; ++t) {
+                        const int m = p + 16 * t;
+                        b[u][t] = row[(m < M ? m : M - 1) >> 1];   // a valid byte; masked below
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < RU; ++u) {
+                if (r0 + 4 * u >= c) break;   // uniform
+                float acc = 0.0f;
+#pragma unroll
+                for (int t = 0; t < T; ++t) {
+                    const int m = p + 16 * t;
+                    if (m < M) acc = acc + lut[m * 16 + ((b[u][t] >> (4 * (m & 1))) & 15u)];
+                }
+                acc = acc + from_lane_minus_f<8>(acc);
+                acc = acc + from_lane_minus_f<4>(acc);
+                acc = acc + from_lane_minus_f<2>(acc);
+                acc = acc + from_lane_minus_f<1>(acc);
+                const int cj = r0 + 4 * u + g;
+                if (p == 15 && cj < c) cd[cj] = acc;
+            }
+        }
+    }
+};
+
+// Exact squared distance of one point to the query, computed by one lane in
+// the fixed order of the float32 path (16 partials over 4-dimension chunks,
+// then pairwise), or exactly in int32 for uint8 vectors: the re-rank of a
+// product-quantised search.
+__device__ __forceinline__ float exact_dist_lane(const void *V, const void *Q, uint32_t qi, uint32_t id, int d,
+                                                 bool u8)
+{
+    if (u8) {
+        const uint4 *x = reinterpret_cast<const uint4 *>(reinterpret_cast<const uint8_t *>(V) + (size_t)id * d);
+        const uint4 *q = reinterpret_cast<const uint4 *>(reinterpret_cast<const uint8_t *>(Q) + (size_t)qi * d);
+        int32_t s = 0;
+        for (int c = 0; c < (d >> 4); ++c) {
+            const uint4 a = x[c], b = q[c];
+            const uint32_t wa[4] = {a.x, a.y, a.z, a.w}, wb[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+            for (int w = 0; w < 4; ++w)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int32_t t = (int32_t)((wa[w] >> (8 * i)) & 0xFF) - (int32_t)((wb[w] >> (8 * i)) & 0xFF);
+                    s += t * t;
+                }
+        }
+        return (float)s;
+    }
+    const float4 *x = reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(V) + (size_t)id * d);
+    const float4 *q = reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(Q) + (size_t)qi * d);
+    const int nch = d >> 2;
+    float acc[16];
+#pragma unroll
+    for (int pp = 0; pp < 16; ++pp) acc[pp] = 0.0f;
+    for (int c0 = 0; c0 < nch; c0 += 16) {
+#pragma unroll
+        for (int pp = 0; pp < 16; ++pp) {
+            if (c0 + pp < nch) {
+                const float4 a = x[c0 + pp], b = q[c0 + pp];
+                float t = a.x - b.x;
+                acc[pp] = __builtin_fmaf(t, t, acc[pp]);
+                t = a.y - b.y;
+                acc[pp] = __builtin_fmaf(t, t, acc[pp]);
+                t = a.z - b.z;
+                acc[pp] = __builtin_fmaf(t, t, acc[pp]);
+                t = a.w - b.w;
+                acc[pp] = __builtin_fmaf(t, t, acc[pp]);
+            }
+        }
+    }
+#pragma unroll
+    for (int st = 8; st >= 1; st >>= 1)
+#pragma unroll
+        for (int pp = 0; pp < st; ++pp) acc[pp] = acc[pp] + acc[pp + st];
+    return acc[0];
+}
+
+__device__ __forceinline__ uint64_t wave_min64(uint64_t v)
+{
+#pragma unroll
+    for (int s = 32; s >= 1; s >>= 1) {
+        const uint64_t o = ((uint64_t)(uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), s) << 32) |
+                           (uint32_t)__shfl_xor((int)(uint32_t)v, s);
+        v = o < v ? o : v;
+    }
+    return v;
+}
 
 // ---------------------------------------------------------------------------
 // Visited set (exact). LDS part: a two-choice bucketed table of 16-bit
@@ -475,8 +639,10 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     uint64_t *posbm = nkey + 64;                                 // pw >= L/64 + 2
     uint32_t *cid = reinterpret_cast<uint32_t *>(posbm + pw);   // 64
     float *cd = reinterpret_cast<float *>(cid + 64);             // 64
-    unsigned char *qlds = reinterpret_cast<unsigned char *>(cd + 64);   // the scorer's query copy, if any
-    uint32_t *htab = reinterpret_cast<uint32_t *>(qlds + Scorer::kLdsBytes);   // H/2 words (H 16-bit slots)
+    unsigned char *qlds = reinterpret_cast<unsigned char *>(cd + 64);   // the scorer's query copy or table
+    // the exact re-rank keys of a product-quantised search (Lb entries)
+    uint64_t *rrk = reinterpret_cast<uint64_t *>(qlds + Scorer::kLdsBytes);
+    uint32_t *htab = reinterpret_cast<uint32_t *>(rrk + (Scorer::kPQ ? Lb : 0));   // H/2 words (H 16-bit slots)
 
     const IndexView ix = a.ix;
     const int R = ix.R, d = ix.d, m = ix.m;
@@ -497,6 +663,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
 
     Scorer sc;
     sc.bind_lds(qlds);
+    if constexpr (Scorer::kPQ) sc.bind_pq(a.pq_codes, a.pq_m, a.pq_cb, d, a.vec_u8);
     // one point's attribute record (m_pad cells) and its violation count
     auto load_attrs = [&](uint32_t id, int4 &w0, int4 &w1) {
         const int32_t *ar = ix.attrs + (size_t)id * ix.m_pad;
@@ -789,9 +956,45 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         const uint32_t n_valid = lower_bound64(beam, min(len, (uint32_t)L), KEY_PHI1);
         const int k = a.k;
         uint32_t conf = 0;
+        // the result (the first valid entries) and the two distances of Eq. 3
+        uint64_t res_key[2] = {KEY_NONE, KEY_NONE};   // (product-quantised search: lanes' top-k keys)
+        float d_k = 0.f, d_max = 0.f;
+        if constexpr (Scorer::kPQ) {
+            // re-rank the valid entries by exact distance (Sec. III-B step 8):
+            // keys (exact distance bits, id); the k smallest in order by k
+            // rounds of a wave minimum, the largest by one wave maximum
+            for (uint32_t b0 = 0; b0 < n_valid; b0 += 64) {
+                const uint32_t e = b0 + lane;
+                if (e < n_valid) {
+                    const uint32_t id = key_id(beam[e]);
+                    const float dx = exact_dist_lane(a.ix.vectors, a.queries, qi, id, d, a.vec_u8 != 0);
+                    rrk[e] = ((uint64_t)__float_as_uint(dx) << 32) | id;
+                }
+            }
+            wave_sync();
+            uint64_t prev = 0, mx = 0;
+            for (uint32_t i = lane; i < n_valid; i += 64) mx = max(mx, rrk[i]);
+            mx = ~wave_min64(~mx);
+            const int kk = min(k, (int)n_valid);
+            for (int q = 0; q < kk; ++q) {
+                uint64_t mn = KEY_NONE;
+                for (uint32_t i = lane; i < n_valid; i += 64) {
+                    const uint64_t x = rrk[i];
+                    if ((q == 0 || x > prev) && x < mn) mn = x;
+                }
+                mn = wave_min64(mn);
+                if ((q & 63) == lane) res_key[q >> 6] = mn;
+                prev = mn;
+            }
+            if (kk > 0) d_k = __uint_as_float((uint32_t)(prev >> 32));
+            d_max = __uint_as_float((uint32_t)(mx >> 32));
+        } else if (n_valid > (uint32_t)k) {
+            d_k = key_dist(beam[k - 1]);
+            d_max = key_dist(beam[n_valid - 1]);
+        }
         if (n_valid > (uint32_t)k) {
-            double dk = sqrt((double)key_dist(beam[k - 1]));
-            double dmax = sqrt((double)key_dist(beam[n_valid - 1]));
+            double dk = sqrt((double)d_k);
+            double dmax = sqrt((double)d_max);
             double gamma = dmax == 0.0 ? 0.0 : (dmax - dk) / dmax;
             conf = gamma <= a.eps ? 1u : 0u;
         }
@@ -813,9 +1016,15 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                 uint32_t id = BOA_PAD;
                 float dd = __int_as_float(0x7f800000);
                 if ((uint32_t)q < n_valid) {
-                    uint64_t kk = beam[q];
-                    id = key_id(kk);
-                    dd = key_dist(kk);
+                    if constexpr (Scorer::kPQ) {
+                        const uint64_t kk = res_key[q >> 6];
+                        id = (uint32_t)kk;
+                        dd = __uint_as_float((uint32_t)(kk >> 32));
+                    } else {
+                        uint64_t kk = beam[q];
+                        id = key_id(kk);
+                        dd = key_dist(kk);
+                    }
                 }
                 a.ids[(size_t)qi * k + q] = id;
                 a.dists[(size_t)qi * k + q] = dd;
@@ -955,16 +1164,30 @@ static int occupancy_t(int wpb, size_t lds)
         }                                                                    \
     } while (0)
 
-#define BOA_DISPATCH(VEC, DIM, WIDE, CALL)                                   \
+#define BOA_DISPATCH_PQ(PQM, CALL)                                           \
     do {                                                                     \
-        if (WIDE) BOA_DISPATCH_W(VEC, DIM, 2, CALL);                         \
+        int T_ = ((PQM) + 15) / 16;                                          \
+        if (T_ <= 1) { using S_ = PQScorer<1>; CALL; }                       \
+        else if (T_ <= 2) { using S_ = PQScorer<2>; CALL; }                  \
+        else if (T_ <= 4) { using S_ = PQScorer<4>; CALL; }                  \
+        else if (T_ <= 8) { using S_ = PQScorer<8>; CALL; }                  \
+        else if (T_ <= 12) { using S_ = PQScorer<12>; CALL; }                \
+        else { using S_ = PQScorer<16>; CALL; }                              \
+    } while (0)
+
+// product-quantised searches (PQM > 0) take the PQ scorer, which has no
+// wide variant; the others the exact scorer of the vector type
+#define BOA_DISPATCH(VEC, DIM, WIDE, CALL, PQM)                              \
+    do {                                                                     \
+        if ((PQM) > 0) BOA_DISPATCH_PQ(PQM, CALL);                           \
+        else if (WIDE) BOA_DISPATCH_W(VEC, DIM, 2, CALL);                    \
         else BOA_DISPATCH_W(VEC, DIM, 1, CALL);                              \
     } while (0)
 
 hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st, bool wide)
 {
     hipError_t e = hipSuccess;
-    BOA_DISPATCH(vec_dtype, a.ix.d, wide, e = launch_phase_t<S_>(a, blocks, st));
+    BOA_DISPATCH(vec_dtype, a.ix.d, wide, e = launch_phase_t<S_>(a, blocks, st), a.pq ? a.pq_m : 0);
     return e;
 }
 
@@ -974,17 +1197,17 @@ static int scorer_lds_t()
     return Scorer::kLdsBytes;
 }
 
-int scorer_lds_bytes(int vec_dtype, int d, bool wide)
+int scorer_lds_bytes(int vec_dtype, int d, bool wide, int pq_m)
 {
     int r = 0;
-    BOA_DISPATCH(vec_dtype, d, wide, r = scorer_lds_t<S_>());
+    BOA_DISPATCH(vec_dtype, d, wide, r = scorer_lds_t<S_>(), pq_m);
     return r;
 }
 
-int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds, bool wide)
+int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds, bool wide, int pq_m)
 {
     int r = 0;
-    BOA_DISPATCH(vec_dtype, d, wide, r = occupancy_t<S_>(wpb, lds));
+    BOA_DISPATCH(vec_dtype, d, wide, r = occupancy_t<S_>(wpb, lds), pq_m);
     return r;
 }
 

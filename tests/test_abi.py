@@ -34,9 +34,9 @@ def test_library_exports_every_declared_symbol():
 def test_struct_layouts_match_header():
     # sizes follow from the header's field order on x86-64
     # k, L0, Lmax, pad, alpha, eps, tau, fixed_L, boa_plus, sub_batches,
-    # lds_hash_slots, schedule, n_schedule, fused, warm_start, tail pad
+    # lds_hash_slots, schedule, n_schedule, fused, warm_start, pq
     assert C.sizeof(boa.Params) == 4 * 3 + 4 + 8 * 3 + 4 * 4 + 8 + 4 + 4 + 4 + 4
-    assert boa.Params.warm_start.offset == 72
+    assert boa.Params.warm_start.offset == 72 and boa.Params.pq.offset == 76
     assert C.sizeof(boa.PhaseStats) == 4 * 4 + 8 * 2 + 8 + 4 + 4
 
 
