@@ -258,6 +258,10 @@ def main():
     ap.add_argument("--graph-cache", default="", help="npz file: load the graph if present, else save it")
     ap.add_argument("--vector-graph", action="store_true",
                     help="build the graph from vector distances only (no attribute-aware edges)")
+    ap.add_argument("--pq", action="store_true",
+                    help="traverse with product-quantised distances (4-bit codes, trained offline) and "
+                         "re-rank exactly (Alg. 2 PQDist; Sec. III-B)")
+    ap.add_argument("--pq-m", type=int, default=0, help="PQ subspaces (default d / 4)")
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -329,11 +333,24 @@ def main():
         f"{np.median(n_valid) / wl.n:.4f}, min valid {int(n_valid.min())}")
 
     index = boa.Index(data.vectors, data.attrs, types, adj, entry)
+    pq_info = None
+    if args.pq:
+        from workloads import pq as pqmod
+        t = time.time()
+        M = args.pq_m or wl.d // 4
+        codebook = pqmod.train(data.vectors, M, seed=wl.seed, device=dev)
+        codes = pqmod.encode(data.vectors, codebook, device=dev)
+        index.set_pq(codebook, codes)
+        pq_info = {"subspaces": M, "centroids": 16, "code_bytes": M // 2,
+                   "bytes_per_scored_node": M // 2 + 4 * wl.m,
+                   "exact_bytes_per_scored_node": wl.d * (1 if wl.vec_dtype == gen.VEC_U8 else 4) + 4 * wl.m}
+        log(f"product quantisation: {M} subspaces x 16 centroids, {M // 2} B codes, trained and encoded "
+            f"in {time.time() - t:.1f}s")
     q = torch.from_numpy(data.queries).to(dev)
     r = torch.from_numpy(data.ranges).to(dev)
     q_ho = torch.from_numpy(ho_q).to(dev)
     r_ho = torch.from_numpy(ho_r).to(dev)
-    base_kw = dict(k=wl.k, L0=wl.L0, Lmax=wl.Lmax, lds_hash_slots=args.lds_slots)
+    base_kw = dict(k=wl.k, L0=wl.L0, Lmax=wl.Lmax, lds_hash_slots=args.lds_slots, pq=args.pq)
 
     def timed(search_kw, steps, warmup, qq=q, rr=r):
         """warm-up, then `steps` timed searches bracketed by device syncs;
@@ -493,7 +510,7 @@ def main():
         widths = doubling_widths(wl.L0, wl.Lmax)
         need = np.full(wl.nq, np.iinfo(np.int32).max, dtype=np.int64)
         for Lw in reversed(widths):
-            o = index.search(q, r, k=wl.k, fixed_L=Lw)
+            o = index.search(q, r, k=wl.k, fixed_L=Lw, pq=args.pq)
             rq_w = eval_recall(o, per_query=True)
             need[rq_w >= 1.0 - 1e-9] = Lw
         lneed = {"widths": widths,
@@ -505,7 +522,7 @@ def main():
 
     fixed = None
     if not args.no_fixed:
-        msf, stf, out_f = timed(dict(k=wl.k, fixed_L=500), args.fixed_steps, 1)
+        msf, stf, out_f = timed(dict(k=wl.k, fixed_L=500, pq=args.pq), args.fixed_steps, 1)
         rs, rt = eval_recall(out_f)
         fixed = dict(L=500, ms_per_step=round(msf, 4), qps=round(wl.nq / (msf / 1e3), 1),
                      recall_at_10=round(rt, 5), recall_at_10_strict=round(rs, 5),
@@ -540,7 +557,8 @@ def main():
         # the CPUs this process may run on (the GPU machine gives each GPU a share
         # of the host; nproc counts the whole host), at most 16
         threads = max(1, min(16, ci["affinity"]))
-        oix = oracle.Index(data.vectors, data.attrs, types, adj, entry)
+        oix = oracle.Index(data.vectors, data.attrs, types, adj, entry,
+                           *((codebook, codes) if args.pq else (None, None)))
         osched = oracle.schedule(wl.L0, chosen["alpha"], wl.Lmax)
 
         def run_oracle(n_q, nt):
@@ -602,6 +620,7 @@ def main():
         "dtype": "f32" if wl.vec_dtype == gen.VEC_F32 else "u8",
         "data": "synthetic",
         "config": {"workload": wl.name, "n": wl.n, "d": wl.d, "R": wl.R, "m": wl.m, "nq": wl.nq,
+                   "distance": "product-quantised traversal, exact re-rank" if args.pq else "exact",
                    "k": wl.k, "L0": wl.L0, "Lmax": wl.Lmax, "alpha": chosen["alpha"], "eps": chosen["eps"],
                    "schedule": sched, "escalation": chosen["escalation"],
                    "mode": f"BOA ({mode} phases)" if mode != "warm" else "BOA (warm-start escalation, fused)",
@@ -637,6 +656,7 @@ def main():
                      "avg_launch_ms": round(avg_launch_ms, 5), "launches": dom["launches"],
                      "launch_groups": groups},
         "cpu_baseline": cpu,
+        "product_quantisation": pq_info,
     }
     line = json.dumps(res)
     print(line, flush=True)

@@ -12,8 +12,8 @@ Layout shared by every consumer:
     subspace 2b + 1 in its high nibble.
 
 Training: k-means (Lloyd, a fixed number of iterations) per subspace on a
-seeded sample, initialised from seeded sample points; encoding: the nearest
-centroid in float64, ties to the lowest index.
+seeded sample, initialised from seeded sample points (torch, all subspaces
+at once); encoding: the nearest centroid, ties to the lowest index.
 """
 from __future__ import annotations
 
@@ -26,44 +26,52 @@ def _rng(seed: int) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0x50])))
 
 
-def train(vectors: np.ndarray, M: int, seed: int = 0, sample: int = 65536, iters: int = 16) -> np.ndarray:
-    """Codebook (M x 16 x ds float32) by k-means per subspace."""
+def _torch_dev(device):
+    import torch
+    dev = torch.device(device)
+    return torch, dev, (torch.float64 if dev.type == "cpu" else torch.float32)
+
+
+def train(vectors: np.ndarray, M: int, seed: int = 0, sample: int = 65536, iters: int = 16,
+          device: str = "cpu") -> np.ndarray:
+    """Codebook (M x 16 x ds float32) by k-means, all subspaces at once
+    (float64 on the CPU, float32 on a GPU)."""
+    torch, dev, dt = _torch_dev(device)
     n, d = vectors.shape
     assert d % M == 0 and M % 2 == 0
     ds = d // M
     g = _rng(seed)
     idx = np.sort(g.choice(n, min(sample, n), replace=False))
-    X = vectors[idx].astype(np.float64).reshape(len(idx), M, ds)
-    cb = np.empty((M, K, ds), dtype=np.float64)
-    for m in range(M):
-        x = X[:, m, :]
-        c = x[g.choice(len(x), K, replace=len(x) < K)].copy()
-        for _ in range(iters):
-            d2 = ((x[:, None, :] - c[None, :, :]) ** 2).sum(-1)
-            a = d2.argmin(1)
-            for j in range(K):
-                sel = a == j
-                if sel.any():
-                    c[j] = x[sel].mean(0)
-        cb[m] = c
-    return cb.astype(np.float32)
+    S = len(idx)
+    X = torch.from_numpy(vectors[idx].astype(np.float32)).to(dev).to(dt).reshape(S, M, ds)
+    init = g.choice(S, K, replace=S < K)
+    C = X[torch.from_numpy(init).to(dev)].permute(1, 0, 2).contiguous()    # M x K x ds
+    ar = torch.arange(M, device=dev)
+    for _ in range(iters):
+        d2 = ((X[:, :, None, :] - C[None, :, :, :]) ** 2).sum(-1)          # S x M x K
+        a = d2.argmin(-1)                                                   # S x M
+        flat = (ar[None, :] * K + a).reshape(-1)
+        sums = torch.zeros((M * K, ds), dtype=dt, device=dev).index_add_(0, flat, X.reshape(-1, ds))
+        cnt = torch.zeros(M * K, dtype=dt, device=dev).index_add_(0, flat, torch.ones_like(flat, dtype=dt))
+        upd = sums / cnt.clamp_min(1)[:, None]
+        keep = (cnt == 0)[:, None]
+        C = torch.where(keep, C.reshape(M * K, ds), upd).reshape(M, K, ds)
+    return C.cpu().numpy().astype(np.float32)
 
 
-def encode(vectors: np.ndarray, codebook: np.ndarray, chunk: int = 1 << 16) -> np.ndarray:
-    """n x M/2 packed 4-bit codes: the nearest centroid per subspace (float64,
-    ties to the lowest index)."""
+def encode(vectors: np.ndarray, codebook: np.ndarray, chunk: int = 1 << 14, device: str = "cpu") -> np.ndarray:
+    """n x M/2 packed 4-bit codes: the nearest centroid per subspace (ties
+    to the lowest index; float64 on the CPU, float32 on a GPU)."""
+    torch, dev, dt = _torch_dev(device)
     n, d = vectors.shape
     M, k, ds = codebook.shape
-    cb = codebook.astype(np.float64)
+    cb = torch.from_numpy(codebook).to(dev).to(dt)
     out = np.empty((n, M // 2), dtype=np.uint8)
     for s in range(0, n, chunk):
         e = min(n, s + chunk)
-        x = vectors[s:e].astype(np.float64).reshape(e - s, M, ds)
-        codes = np.empty((e - s, M), dtype=np.uint8)
-        for m in range(M):
-            d2 = ((x[:, m, None, :] - cb[m][None, :, :]) ** 2).sum(-1)
-            codes[:, m] = d2.argmin(1)
-        out[s:e] = codes[:, 0::2] | (codes[:, 1::2] << 4)
+        x = torch.from_numpy(vectors[s:e].astype(np.float32)).to(dev).to(dt).reshape(e - s, M, ds)
+        c = ((x[:, :, None, :] - cb[None]) ** 2).sum(-1).argmin(-1).to(torch.uint8).cpu().numpy()
+        out[s:e] = c[:, 0::2] | (c[:, 1::2] << 4)
     return out
 
 
