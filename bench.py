@@ -252,8 +252,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle timing")
     ap.add_argument("--lds-slots", type=int, default=0, help="force the LDS visited-table size")
-    ap.add_argument("--modes", default="phased,fused,split,boa_plus",
-                    help="adaptive modes to time; the fastest is the headline")
+    ap.add_argument("--modes", default="phased,fused,split,boa_plus,warm",
+                    help="adaptive modes to time (warm: warm-start escalation, fused); the fastest of the "
+                         "escalation kind chosen on the held-out batch is the headline")
+    ap.add_argument("--no-paper", action="store_true", help="skip the paper's operating point")
     ap.add_argument("--json-out", default="")
     ap.add_argument("--graph-cache", default="", help="npz file: load the graph if present, else save it")
     ap.add_argument("--vector-graph", action="store_true",
@@ -385,7 +387,12 @@ def main():
     # two kinds of escalation: each phase restarting the search (Alg. 1 as
     # printed; timed in split mode here) or continuing from the previous
     # phase's state (warm start, fused mode)
+    mode_list = args.modes.split(",")
     kinds = {"restart": {"split": True}, "warm": {"fused": True, "warm": True}}
+    if "warm" not in mode_list:
+        del kinds["warm"]
+    if not [m2 for m2 in mode_list if m2 != "warm"]:
+        del kinds["restart"]
     points = [(e, a, kd) for kd in kinds for a in alpha_grid for e in eps_grid]
     sweep = []
     for e, a, kd in points:
@@ -416,27 +423,30 @@ def main():
                "warm": {"fused": True, "warm": True}}
     kw_kind = {kd: dict(base_kw, eps=c["eps"], alpha=c["alpha"]) for kd, c in chosen_kind.items()}
     modes = {}
-    for mode in args.modes.split(",") + ["warm"]:
+    for mode in mode_list:
         kd = "warm" if mode == "warm" else "restart"
         ms_m, st_m, out_m = timed(dict(kw_kind[kd], **mode_kw[mode]), args.steps, args.warmup)
         modes[mode] = (ms_m, st_m, out_m)
         log(f"adaptive ({mode}, eps={kw_kind[kd]['eps']} alpha={kw_kind[kd]['alpha']}): {ms_m:.3f} ms/step, "
             f"{wl.nq / (ms_m / 1e3):,.0f} QPS")
     restart_modes = [m2 for m2 in modes if m2 != "warm"]
-    ids_r = modes[restart_modes[0]][2].ids.cpu().numpy().view(np.uint32)
-    for m2 in restart_modes:
-        assert np.array_equal(modes[m2][2].ids.cpu().numpy().view(np.uint32), ids_r), f"{m2} results differ"
+    if restart_modes:
+        ids_r = modes[restart_modes[0]][2].ids.cpu().numpy().view(np.uint32)
+        for m2 in restart_modes:
+            assert np.array_equal(modes[m2][2].ids.cpu().numpy().view(np.uint32), ids_r), f"{m2} results differ"
     mode = "warm" if chosen["escalation"] == "warm" else min(restart_modes, key=lambda k2: modes[k2][0])
     kw = kw_kind[chosen["escalation"]]
     ms, st, out = modes[mode]
     qps = wl.nq / (ms / 1e3)
+    other_kind = None
     other = "restart" if mode == "warm" else "warm"
-    om = "warm" if other == "warm" else min(restart_modes, key=lambda k2: modes[k2][0])
-    rs_o, rt_o = eval_recall(modes[om][2])
-    other_kind = dict(escalation=other, mode=om, eps=kw_kind[other]["eps"], alpha=kw_kind[other]["alpha"],
-                      ms_per_step=round(modes[om][0], 4), qps=round(wl.nq / (modes[om][0] / 1e3), 1),
-                      recall_at_10=round(rt_o, 5), recall_at_10_strict=round(rs_o, 5),
-                      L_avg=round(float(modes[om][2].final_L.cpu().numpy().mean()), 2))
+    if other in kinds:
+        om = "warm" if other == "warm" else min(restart_modes, key=lambda k2: modes[k2][0])
+        rs_o, rt_o = eval_recall(modes[om][2])
+        other_kind = dict(escalation=other, mode=om, eps=kw_kind[other]["eps"], alpha=kw_kind[other]["alpha"],
+                          ms_per_step=round(modes[om][0], 4), qps=round(wl.nq / (modes[om][0] / 1e3), 1),
+                          recall_at_10=round(rt_o, 5), recall_at_10_strict=round(rs_o, 5),
+                          L_avg=round(float(modes[om][2].final_L.cpu().numpy().mean()), 2))
 
     ids = out.ids.cpu().numpy().view(np.uint32)
     final_L = out.final_L.cpu().numpy()
@@ -520,6 +530,28 @@ def main():
                  "pct_escalated_past_L_needed": round(100.0 * float((final_L > need).mean()), 2)}
         log(f"L needed: {lneed}")
 
+    def paper_leg(pmode):
+        """the paper's own point (eps 0.05, alpha 2; Sec. IV) on the
+        evaluation batch, restarting (in pmode) and with warm start"""
+        msp, stp, out_p = timed(dict(base_kw, eps=0.05, alpha=2.0, **mode_kw[pmode]), args.fixed_steps, 1)
+        rps, rpt = eval_recall(out_p)
+        paper_point = dict(eps=0.05, alpha=2.0, mode=pmode, schedule=[p["L"] for p in stp["phases"]],
+                           ms_per_step=round(msp, 4), qps=round(wl.nq / (msp / 1e3), 1), recall_at_10=round(rpt, 5),
+                           recall_at_10_strict=round(rps, 5),
+                           L_avg=round(float(out_p.final_L.cpu().numpy().mean()), 2),
+                           speedup_vs_fixed_L500=round((wl.nq / (msp / 1e3)) / fixed["qps"], 3)
+                           if fixed else None)
+        log(f"paper's point eps=0.05 alpha=2 ({pmode}): {msp:.3f} ms/step, recall {rpt:.4f}")
+        # the same point with warm-start escalation
+        msw, _, out_w = timed(dict(base_kw, eps=0.05, alpha=2.0, **mode_kw["warm"]), args.fixed_steps, 1)
+        _, rwt = eval_recall(out_w)
+        paper_point["warm"] = dict(ms_per_step=round(msw, 4), qps=round(wl.nq / (msw / 1e3), 1),
+                                   recall_at_10=round(rwt, 5),
+                                   L_avg=round(float(out_w.final_L.cpu().numpy().mean()), 2),
+                                   speedup_vs_fixed_L500=round((wl.nq / (msw / 1e3)) / fixed["qps"], 3) if fixed else None)
+        log(f"paper's point with warm start: {msw:.3f} ms/step, recall {rwt:.4f}")
+        return paper_point
+
     fixed = None
     if not args.no_fixed:
         msf, stf, out_f = timed(dict(k=wl.k, fixed_L=500, pq=args.pq), args.fixed_steps, 1)
@@ -531,24 +563,11 @@ def main():
 
     # the paper's own point (eps 0.05, alpha 2; Sec. IV), on the evaluation
     # batch, in the fastest mode
-    pmode = min(restart_modes, key=lambda k2: modes[k2][0])
-    msp, stp, out_p = timed(dict(base_kw, eps=0.05, alpha=2.0, **mode_kw[pmode]), args.fixed_steps, 1)
-    rps, rpt = eval_recall(out_p)
-    paper_point = dict(eps=0.05, alpha=2.0, mode=pmode, schedule=[p["L"] for p in stp["phases"]],
-                       ms_per_step=round(msp, 4), qps=round(wl.nq / (msp / 1e3), 1), recall_at_10=round(rpt, 5),
-                       recall_at_10_strict=round(rps, 5),
-                       L_avg=round(float(out_p.final_L.cpu().numpy().mean()), 2),
-                       speedup_vs_fixed_L500=round((wl.nq / (msp / 1e3)) / fixed["qps"], 3)
-                       if fixed else None)
-    log(f"paper's point eps=0.05 alpha=2 ({pmode}): {msp:.3f} ms/step, recall {rpt:.4f}")
-    # the same point with warm-start escalation
-    msw, _, out_w = timed(dict(base_kw, eps=0.05, alpha=2.0, **mode_kw["warm"]), args.fixed_steps, 1)
-    _, rwt = eval_recall(out_w)
-    paper_point["warm"] = dict(ms_per_step=round(msw, 4), qps=round(wl.nq / (msw / 1e3), 1),
-                               recall_at_10=round(rwt, 5),
-                               L_avg=round(float(out_w.final_L.cpu().numpy().mean()), 2),
-                               speedup_vs_fixed_L500=round((wl.nq / (msw / 1e3)) / fixed["qps"], 3) if fixed else None)
-    log(f"paper's point with warm start: {msw:.3f} ms/step, recall {rwt:.4f}")
+    paper_point = None
+    if not args.no_paper:
+        pmode = min(restart_modes, key=lambda k2: modes[k2][0]) if restart_modes else "split"
+        paper_point = paper_leg(pmode)
+
 
     cpu = None
     if not args.no_cpu_baseline:
