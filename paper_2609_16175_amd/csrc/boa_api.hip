@@ -118,8 +118,10 @@ struct boa_index {
     uint8_t *qstat = nullptr;        // ph_cap x nq
     uint32_t *qE = nullptr, *qS = nullptr;  // ph_cap x nq
     uint32_t *status = nullptr;
-    uint32_t *bits = nullptr;        // visited spill bitmaps, bits_words per wave slot
+    uint32_t *bits = nullptr;        // visited spill bitmaps and their logs, slot_words per wave slot
     uint32_t bits_words = 0;
+    uint32_t slot_words = 0, log_cap = 0;
+    bool logs_fresh = false;         // the logs' headers are not yet set (next search sets them)
     uint64_t slots_cap = 0;
     uint32_t *pool = nullptr;        // BOA+ survivor pools (ph_cap x nq)
     hipStream_t aux = nullptr;       // BOA+ second stream
@@ -355,6 +357,21 @@ int ensure_events(boa_index *ix, size_t count)
     return BOA_OK;
 }
 
+// A wave slot's spill bitmap: one bit per point, whole 16-byte units.
+uint32_t bitmap_words(const boa_index *ix)
+{
+    return (uint32_t)(((ix->view.n + 127) / 128) * 4);
+}
+
+// Ids the spill log holds: clearing by the log writes about one 64-byte
+// line per logged id, so it pays while the log is under 1/16 of the
+// bitmap's words; at most 16380 (a 64 KB log); none for small bitmaps.
+uint32_t spill_log_cap(uint32_t bits_words)
+{
+    uint32_t c = std::min<uint32_t>(bits_words / 16u, 16380u) & ~3u;
+    return c < 64u ? 0u : c;
+}
+
 int ensure_workspace(boa_index *ix, int64_t nq, int32_t n_phases, uint64_t slots, int32_t n_counters, bool plus)
 {
     int rc;
@@ -389,17 +406,23 @@ int ensure_workspace(boa_index *ix, int64_t nq, int32_t n_phases, uint64_t slots
         ix->n_counters = n_counters;
     }
     if (slots > ix->slots_cap) {
-        // one bit per point per wave slot, in whole 16-byte units; a query
-        // zeroes its slot's bitmap when it first spills, so no clearing here
+        // one bit per point per wave slot, in whole 16-byte units, and the
+        // log of the bits set; a query clears its slot's bitmap when it first
+        // spills (by the log, or whole when the log's header says so), so no
+        // clearing here: the next search marks every header unknown first
         uint64_t sc = std::max<uint64_t>(slots, ix->slots_cap);
-        uint32_t words = (uint32_t)(((ix->view.n + 127) / 128) * 4);
+        const uint32_t words = bitmap_words(ix);
+        const uint32_t cap = spill_log_cap(words);
         dfree(ix->bits);
-        if ((rc = dalloc(&ix->bits, (size_t)sc * words))) {
+        if ((rc = dalloc(&ix->bits, (size_t)sc * (words + BOA_LOG_HDR + cap)))) {
             ix->slots_cap = 0;
             return rc;
         }
         ix->slots_cap = sc;
         ix->bits_words = words;
+        ix->log_cap = cap;
+        ix->slot_words = words + BOA_LOG_HDR + cap;
+        ix->logs_fresh = true;
     }
     if (plus && !ix->aux) {
         HIP_TRY(hipStreamCreateWithFlags(&ix->aux, hipStreamNonBlocking));
@@ -595,8 +618,10 @@ struct Workspace {
     uint8_t *qstat;           // per phase x nq, with qE and qS (null: no per-phase statistics)
     uint32_t *qE, *qS;
     uint32_t *status;
-    uint32_t *bits;           // visited spill bitmaps, bits_words u32 per wave slot
-    uint32_t bits_words;
+    uint32_t *bits;           // visited spill bitmaps and logs, slot_words u32 per wave slot
+    uint32_t bits_words, slot_words, log_cap;
+    bool reset_logs;          // the logs' headers must be marked unknown before the search
+    bool *logs_fresh;         // cleared once that reset is enqueued (null: reset every search)
     uint64_t slots;           // wave slots that have a spill bitmap
     uint32_t *pool;           // BOA+ survivor pools, 2 nq (null: no BOA+)
     bool timing;              // HIP events around launches; statistics of the search kept
@@ -665,8 +690,14 @@ int plan_search(const boa_index *ix, const Request &rq, int64_t nq, int32_t forc
     const int32_t Lw = rq.sched[rq.n_phases - 1];
     for (int32_t ph = 0; ph < rq.n_phases; ++ph) {
         // a fused launch, and a BOA+ escalation launch, size LDS for the widest phase
-        const bool wide = rq.fused || (rq.plus && ph > 0);
-        PhasePlan pl = plan_phase_widest(ix, wide ? Lw : rq.sched[ph], forced_h, nq, false, rq.pq_m);
+        const bool widest = rq.fused || (rq.plus && ph > 0);
+        PhasePlan pl = plan_phase_widest(ix, widest ? Lw : rq.sched[ph], forced_h, nq, false, rq.pq_m);
+        if (rq.fused && Lw > 64) {
+            // the wide variant (eight-way worklist search, more rows in
+            // flight) wherever it keeps as many waves resident
+            const PhasePlan w = plan_phase_widest(ix, Lw, forced_h, nq, true, rq.pq_m);
+            if (w.capacity >= pl.capacity && (size_t)w.lds_per_wave <= ix->lds_per_block_max) pl = w;
+        }
         pl.L = rq.sched[ph];
         if ((size_t)pl.lds_per_wave > ix->lds_per_block_max)
             return fail(BOA_EUNSUPPORTED, "beamwidth too wide for the LDS budget");
@@ -719,6 +750,10 @@ int run_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_
     ia.nq = nq;
     ia.n_phases = n_phases;
     ia.n_counters = rq.n_counters;
+    ia.bits = ws.bits;
+    ia.slot_words = ws.slot_words;
+    ia.bits_words = ws.bits_words;
+    ia.reset_slots = ws.reset_logs ? ws.slots : 0;
 
     if (ws.timing) {
         ix->launch_phase.clear();
@@ -726,6 +761,7 @@ int run_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_
     }
     ix->have_stats = false;
     HIP_TRY(launch_init(ia, st));
+    if (ws.reset_logs && ws.logs_fresh) *ws.logs_fresh = false;
 
     PhaseArgs base{};
     base.ix = ix->view;
@@ -738,6 +774,8 @@ int run_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_
     base.user_S = scored;
     base.bits = ws.bits;
     base.bits_words = ws.bits_words;
+    base.slot_words = ws.slot_words;
+    base.log_cap = ws.log_cap;
     base.id_bits = id_bits(ix);
     base.status = ws.status;
     base.eps = p->eps;
@@ -783,7 +821,18 @@ int run_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_
         a.lds_per_wave = pl.lds_per_wave;
         a.waves_per_block = pl.wpb;
         a.slot_base = 0;
-        if (int rc = launch(a, pl.blocks, st, false, 0)) return rc;
+#ifdef BOA_STAGE_PROFILE
+        unsigned long long *prof = nullptr;
+        const size_t pn = (size_t)pl.blocks * pl.wpb * BOA_PROF_SLOTS;
+        if (int rc2 = stage_profile_begin(&prof, pn, st)) return rc2;
+        a.prof = prof;
+#endif
+        if (int rc = launch(a, pl.blocks, st, pl.wide, 0)) return rc;
+#ifdef BOA_STAGE_PROFILE
+        std::fprintf(stderr, "[stage-profile] fused launch%s: table %d slots, %d waves (all phases)\n",
+                     rq.warm ? " (warm start)" : "", pl.h_slots, pl.blocks * pl.wpb);
+        if (int rc2 = stage_profile_end(prof, pn, Lw, pl.blocks * pl.wpb, st)) return rc2;
+#endif
         pl.launches = 1;
     } else if (rq.split) {
         // the first phase over every query at its own width ...
@@ -1066,6 +1115,10 @@ extern "C" int boa_search(boa_index *ix, const void *queries, const int32_t *ran
     ws.status = ix->status;
     ws.bits = ix->bits;
     ws.bits_words = ix->bits_words;
+    ws.slot_words = ix->slot_words;
+    ws.log_cap = ix->log_cap;
+    ws.reset_logs = ix->logs_fresh;
+    ws.logs_fresh = &ix->logs_fresh;
     ws.slots = ix->slots_cap;
     ws.pool = ix->pool;
     ws.timing = true;
@@ -1111,9 +1164,14 @@ extern "C" int boa_search_noalloc(boa_index *ix, const void *queries, const int3
     ws.qE = ws.qS = nullptr;
     ws.pool = nullptr;
     ws.timing = false;
-    ws.bits_words = (uint32_t)(((ix->view.n + 127) / 128) * 4);
+    ws.bits_words = bitmap_words(ix);
+    ws.log_cap = spill_log_cap(ws.bits_words);
+    ws.slot_words = ws.bits_words + BOA_LOG_HDR + ws.log_cap;
+    // (the carve-out moves with nq: no log header of an earlier call is trusted)
+    ws.reset_logs = true;
+    ws.logs_fresh = nullptr;
     ws.bits = reinterpret_cast<uint32_t *>(base + off);
-    ws.slots = off < kScratchBytes ? (kScratchBytes - off) / ((size_t)ws.bits_words * 4) : 0;
+    ws.slots = off < kScratchBytes ? (kScratchBytes - off) / ((size_t)ws.slot_words * 4) : 0;
     if (ws.slots > slots) ws.slots = slots;
     return run_search(ix, queries, ranges, nq, p, rq, plans, ids, dists, final_L, expansions, scored, ws, st);
 }

@@ -9,6 +9,11 @@
 #define BOA_PAD 0xFFFFFFFFu
 #define BOA_STATUS_OVERFLOW 1u
 #define BOA_PROF_SLOTS 16
+// Spill-bitmap log: a wave slot's bitmap is followed by a 4-word header
+// (word 0: the number of logged ids, or BOA_LOG_DIRTY) and the ids whose
+// bits were set since the bitmap was last clear.
+#define BOA_LOG_HDR 4u
+#define BOA_LOG_DIRTY 0xFFFFFFFFu
 
 namespace boa {
 
@@ -40,8 +45,10 @@ struct PhaseArgs {
     uint32_t *qE, *qS;        // [phase][query]: expansions, scored
     int64_t nq;               // stride of the per-phase arrays
     uint32_t *user_E, *user_S;// optional per-query totals over phases
-    uint32_t *bits;           // visited spill bitmaps, bits_words u32 per wave slot
-    uint32_t bits_words;
+    uint32_t *bits;           // per wave slot (slot_words u32): spill bitmap, then its log
+    uint32_t bits_words;      // bitmap words (a multiple of 4)
+    uint32_t slot_words;      // bits_words + BOA_LOG_HDR + log_cap
+    uint32_t log_cap;         // ids the log holds (0: no log, every clear is whole)
     uint32_t *status;
     double eps;
     uint32_t tau_count;       // the phase runs only if n_active > tau_count
@@ -92,6 +99,11 @@ struct InitArgs {
     int64_t nq;
     int32_t n_phases;
     int32_t n_counters;
+    // spill-log headers of the first reset_slots wave slots set to
+    // BOA_LOG_DIRTY (their bitmaps' contents unknown)
+    uint32_t *bits;
+    uint32_t slot_words, bits_words;
+    uint64_t reset_slots;
 };
 
 // Index construction (boa_build.hip): the medoid entry point, and the graph

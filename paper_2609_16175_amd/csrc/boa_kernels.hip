@@ -141,6 +141,10 @@ template <int T, int W = 1>
 struct F32Scorer {
     // lane p = lane & 15 accumulates float4 chunks p, p+16, p+32, ...
     static constexpr bool kWide = W == 2;
+    static constexpr bool kSpec = false;
+    struct RowGather {};
+    __device__ __forceinline__ void gather_row(const void *, int, uint32_t, int, int, RowGather &) const {}
+    __device__ __forceinline__ void score_row(const RowGather &, int, int, float *, int) const {}
     // rows of more than 320 dimensions keep the query in LDS rather than in
     // 4T registers (every 16-lane group reads the same chunks: broadcasts)
     static constexpr bool kQueryLds = T >= 6;
@@ -261,30 +265,35 @@ struct F32Scorer {
 template <int G, int W = 1>
 struct U8Scorer {
     // lane p = lane % G holds the query's 16-byte chunk p (p < d/16); the
-    // exact int32 sum is order-free.
+    // exact int32 sum is order-free. Per chunk, |x - q|^2 = x.x - 2 x.q + q.q
+    // from unsigned 4-byte dot products: every term is an exact integer
+    // (at most 16 * 255^2 per lane), so the result is the exact sum of
+    // squared differences.
     static constexpr bool kWide = W == 2;
+    // rows of at most 128 bytes gather every neighbour of an expanded node
+    // before its visited test (gather_row / score_row below)
+    static constexpr bool kSpec = G <= 8;
     static constexpr int kLdsBytes = 0;
     static constexpr bool kPQ = false;
     uint4 q;
+    uint32_t qq;   // q.q of this lane's chunk
 
     __device__ __forceinline__ void bind_lds(void *) {}
 
     __device__ __forceinline__ void load_query(const void *Q, uint32_t qi, int d, int lane)
     {
-        const uint8_t *qq = reinterpret_cast<const uint8_t *>(Q) + (size_t)qi * d;
+        const uint8_t *qb = reinterpret_cast<const uint8_t *>(Q) + (size_t)qi * d;
         int p = lane % G;
-        q = p < (d >> 4) ? reinterpret_cast<const uint4 *>(qq)[p] : make_uint4(0, 0, 0, 0);
+        q = p < (d >> 4) ? reinterpret_cast<const uint4 *>(qb)[p] : make_uint4(0, 0, 0, 0);
+        qq = dot16(q, q);
     }
 
-    static __device__ __forceinline__ int32_t sq4(uint32_t a, uint32_t b)
+    static __device__ __forceinline__ uint32_t dot16(const uint4 &a, const uint4 &b)
     {
-        int32_t s = 0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            int32_t da = (int32_t)((a >> (8 * i)) & 0xFF) - (int32_t)((b >> (8 * i)) & 0xFF);
-            s += da * da;
-        }
-        return s;
+        uint32_t s = __builtin_amdgcn_udot4(a.x, b.x, 0u, false);
+        s = __builtin_amdgcn_udot4(a.y, b.y, s, false);
+        s = __builtin_amdgcn_udot4(a.z, b.z, s, false);
+        return __builtin_amdgcn_udot4(a.w, b.w, s, false);
     }
 
     static constexpr int PER = 64 / G;   // candidates per round
@@ -330,12 +339,51 @@ struct U8Scorer {
         }
     }
 
+    // Every neighbour of an expanded node, before its visited test: lane j
+    // holds row entry j (padding replaced by a valid id), and round u's
+    // G-lane group g loads chunk p of entry PER u + g. All rounds' loads are
+    // issued together; score_row waits for them.
+    static constexpr int RS = kSpec ? (BOA_MAX_R + PER - 1) / PER : 1;
+    struct RowGather {
+        uint4 x[RS];
+    };
+
+    __device__ __forceinline__ void gather_row(const void *V, int d, uint32_t v, int R, int lane,
+                                               RowGather &rg) const
+    {
+        const uint8_t *vec = reinterpret_cast<const uint8_t *>(V);
+        const int g = lane / G, p = lane % G, nch = d >> 4;
+        // every round's id first (cross-lane reads in flight together), then
+        // the loads
+        uint32_t id[RS];
+#pragma unroll
+        for (int u = 0; u < RS; ++u) id[u] = (uint32_t)__shfl((int)v, (PER * u + g) & 63);
+#pragma unroll
+        for (int u = 0; u < RS; ++u) {
+            if (PER * u < R)   // uniform
+                rg.x[u] = reinterpret_cast<const uint4 *>(vec + (size_t)id[u] * d)[p < nch ? p : nch - 1];
+        }
+    }
+
+    // distances of the gathered entries: cd[j] for j < R
+    __device__ __forceinline__ void score_row(const RowGather &rg, int d, int R, float *cd, int lane) const
+    {
+        const int g = lane / G, p = lane % G, nch = d >> 4;
+#pragma unroll
+        for (int u = 0; u < RS; ++u) {
+            if (PER * u >= R) break;   // uniform
+            const int32_t acc = dist(rg.x[u], p, nch);
+            const int cj = PER * u + g;
+            if (p == G - 1 && cj < R) cd[cj] = (float)acc;
+        }
+    }
+
     // exact squared distance of one row held by a G-lane group (16-byte
     // chunk p in x); the group's top lane returns it
     __device__ __forceinline__ int32_t dist(uint4 x, int p, int nch) const
     {
         if (p >= nch) x = q;   // lanes past the row: add zero
-        int32_t acc = sq4(x.x, q.x) + sq4(x.y, q.y) + sq4(x.z, q.z) + sq4(x.w, q.w);
+        int32_t acc = (int32_t)(dot16(x, x) + qq - 2u * dot16(x, q));
         // exact integer sum over the group; the group's top lane holds it
 #pragma unroll
         for (int s = G >> 1; s >= 16; s >>= 1) acc += __shfl_xor(acc, s);
@@ -355,6 +403,10 @@ struct U8Scorer {
 template <int T>
 struct PQScorer {
     static constexpr bool kWide = false;
+    static constexpr bool kSpec = false;
+    struct RowGather {};
+    __device__ __forceinline__ void gather_row(const void *, int, uint32_t, int, int, RowGather &) const {}
+    __device__ __forceinline__ void score_row(const RowGather &, int, int, float *, int) const {}
     static constexpr bool kPQ = true;
     static constexpr int kLdsBytes = 16 * T * 16 * 4;   // the table of up to 16 T subspaces
     float *lut = nullptr;
@@ -518,10 +570,15 @@ __device__ __forceinline__ uint64_t wave_min64(uint64_t v)
 // id uniquely. A bucket holds 8 entries (16 bytes, one LDS read).
 // Insert goes to the emptier bucket through a 32-bit CAS on the word that
 // holds the slot. When both buckets are full the id goes to the wave slot's
-// bitmap over all points in HBM (zeroed when a query first overflows).
+// bitmap over all points in HBM (cleared when a query first overflows).
 // Buckets only fill up, so an id absent from a bucket pair that still has
 // room has never been inserted anywhere: the bitmap is consulted only when
 // both buckets are full.
+// The bitmap keeps a log of the ids whose bits were set since it was last
+// clear, so that the clear rewrites only their words; when the log is full
+// (or its state unknown, header BOA_LOG_DIRTY) the whole bitmap is cleared.
+// The wave holds the log's length in a register and writes it back to the
+// header when it exits.
 
 struct Visited {
     uint32_t *words;     // LDS table, 2 entries per word, 4 words per bucket
@@ -530,6 +587,8 @@ struct Visited {
     uint32_t idbits;     // B
     uint32_t *bits;      // this wave slot's HBM bitmap, words32 words
     uint32_t words32;
+    uint32_t *log;       // its log: header word, then (after BOA_LOG_HDR words) log_cap ids
+    uint32_t log_cap;
     uint32_t *status;
 };
 
@@ -609,11 +668,26 @@ __device__ __forceinline__ bool visit_bits(const Visited &s, uint32_t v)
     return (old & bit) == 0u;
 }
 
-__device__ __forceinline__ void clear_bits(const Visited &s, int lane)
+// Clear the bitmap before a query's first spill: the words of the n_log
+// logged ids, or every word when the log does not cover the set bits.
+__device__ __forceinline__ void clear_bits(const Visited &s, uint32_t n_log, int lane)
 {
-    uint4 z = make_uint4(0, 0, 0, 0);
-    uint4 *b4 = reinterpret_cast<uint4 *>(s.bits);
-    for (uint32_t i = lane; i < (s.words32 >> 2); i += 64) b4[i] = z;
+    if (n_log <= s.log_cap) {
+        const uint32_t *ids = s.log + BOA_LOG_HDR;
+        uint32_t i = lane;
+        for (; i + 192 < n_log; i += 256) {   // four loads in flight, then their stores
+            const uint32_t v0 = ids[i], v1 = ids[i + 64], v2 = ids[i + 128], v3 = ids[i + 192];
+            s.bits[v0 >> 5] = 0u;
+            s.bits[v1 >> 5] = 0u;
+            s.bits[v2 >> 5] = 0u;
+            s.bits[v3 >> 5] = 0u;
+        }
+        for (; i < n_log; i += 64) s.bits[ids[i] >> 5] = 0u;
+    } else {
+        uint4 z = make_uint4(0, 0, 0, 0);
+        uint4 *b4 = reinterpret_cast<uint4 *>(s.bits);
+        for (uint32_t i = lane; i < (s.words32 >> 2); i += 64) b4[i] = z;
+    }
     // the stores must land before this wave's atomics on the same words
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
 }
@@ -657,8 +731,13 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     vs.idbits = a.id_bits;
     vs.rbits = a.id_bits > (uint32_t)(a.h_log2 - 3) ? a.id_bits - (uint32_t)(a.h_log2 - 3) : 0u;
     vs.words32 = a.bits_words;
-    vs.bits = a.bits + (size_t)slot * a.bits_words;
+    vs.bits = a.bits + (size_t)slot * a.slot_words;
+    vs.log = vs.bits + a.bits_words;
+    vs.log_cap = a.log_cap;
     vs.status = a.status;
+    // ids logged in this slot's bitmap (its header, kept in a register while
+    // this wave runs: no other wave uses the slot meanwhile)
+    uint32_t n_log = a.vis_bitmap ? 0u : __builtin_amdgcn_readfirstlane(vs.log[0]);
     const uint32_t table_words = a.vis_bitmap ? a.vis_words : (1u << a.h_log2) >> 1;
 
     Scorer sc;
@@ -746,9 +825,22 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             if (__ballot(vst < 0) != 0ull) {
                 if (!spill) {          // first overflow of this query: reset the bitmap
                     spill = true;
-                    clear_bits(vs, lane);
+                    clear_bits(vs, n_log, lane);
+                    n_log = 0;
                 }
-                if (vst < 0) vst = visit_bits(vs, v) ? 1 : 0;
+                const bool to_bits = vst < 0;
+                if (to_bits) vst = visit_bits(vs, v) ? 1 : 0;
+                // log the ids whose bits this wave has just set
+                const uint64_t lm = __ballot(to_bits && vst > 0);
+                if (lm) {
+                    const uint32_t cnt = (uint32_t)__popcll(lm);
+                    if (n_log <= vs.log_cap && cnt <= vs.log_cap - n_log) {
+                        if (to_bits && vst > 0) vs.log[BOA_LOG_HDR + n_log + lanes_below(lm)] = v;
+                        n_log += cnt;
+                    } else {
+                        n_log = BOA_LOG_DIRTY;
+                    }
+                }
             }
             return vst;
         };
@@ -767,16 +859,25 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             else visit_lds(vs, ix.entry);
             cid[0] = ix.entry;
         }
+        // row-gather scorers: the keys of the last expansion's new
+        // neighbours (one per row position, KEY_NONE elsewhere), scored in
+        // that expansion and entered at the top of the next iteration
+        uint32_t spec_c = 0;
+        uint64_t spec_key = KEY_NONE;
 
         for (;;) {
             uint32_t scan_from = (uint32_t)(expanded_j + 1);
             // ---- score the c new candidates listed in cid[0, c)
             PROF_T(t_score0);
-            if (c > 0) {
+            if (c > 0 || spec_c > 0) {
                 wave_sync();
-                S += c;
                 uint64_t key = KEY_NONE;
-                {
+                if (Scorer::kSpec && spec_c > 0) {
+                    S += spec_c;
+                    key = spec_key;
+                    spec_c = 0;
+                } else {
+                    S += c;
                     // attribute records first, then the vectors, so that both
                     // gathers are in flight together; phi is counted afterwards.
                     // This lane's candidate (for its attribute record) and the
@@ -790,6 +891,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                     const uint32_t phi = count_phi(w0, w1);
                     wave_sync();
                     if (lane < (int)c) key = make_key(phi, cd[lane], cid[lane]);
+                    c = 0;
                 }
                 PROF_T(t_score1);
                 PROF_ADD(2, t_score1 - t_score0);
@@ -843,7 +945,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                     }
                     const uint32_t p0 = bcast0(pos);
                     const uint32_t newlen = min((uint32_t)Lcap, len + kept);
-                    const uint32_t w_lo = p0 >> 6, w_hi = (newlen - 1u) >> 6;
+                    const uint32_t w_lo = bcast0(p0 >> 6), w_hi = bcast0((newlen - 1u) >> 6);
                     for (uint32_t w = w_lo + lane; w <= w_hi; w += 64) posbm[w] = 0ull;
                     wave_sync();
                     const bool placed = f < (uint32_t)Lcap;
@@ -854,23 +956,42 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                     PROF_T(t_rank1);
                     PROF_ADD(4, t_rank1 - t_sort1);
                     PROF_ADD(7, w_hi - w_lo + 1);
-                    // rebuild [p0, newlen) from the last 64-slot chunk down
-                    uint64_t word = posbm[w_hi];
-                    uint32_t below = n_placed - (uint32_t)__popcll(word);   // new keys before chunk
-                    for (int w = (int)w_hi; w >= (int)w_lo; --w) {
-                        const uint32_t o = ((uint32_t)w << 6) + lane;
-                        const bool act = o >= p0 && o < newlen;
-                        const bool isnew = (word >> lane) & 1ull;
-                        const uint32_t cnt = below + (uint32_t)__popcll(word & ((1ull << lane) - 1ull));
-                        uint64_t val = 0;
-                        if (act) val = isnew ? nkey[cnt] : beam[o - cnt];
-                        wave_sync();
-                        if (act) beam[o] = val;
-                        if (w > (int)w_lo) {
-                            word = posbm[w - 1];
-                            below -= (uint32_t)__popcll(word);
+                    // rebuild [p0, newlen) from the last 64-slot chunk down, four
+                    // chunks at a time: their reads first (independent), then
+                    // their writes. An entry moves only upwards, so a group's
+                    // writes land above every source of the groups after it.
+                    // Lane i holds chunk w_lo + i's bitmap word (at most 33
+                    // chunks for a width of 2048).
+                    const uint64_t pwl = lane <= (int)(w_hi - w_lo) ? posbm[w_lo + lane] : 0ull;
+                    uint32_t above = 0;   // new keys in the chunks already done
+                    for (uint32_t g = w_hi + 1u; g > w_lo;) {   // g: one past the group's top chunk
+                        const uint32_t ng = min(4u, g - w_lo);
+                        // the group's bitmap words, into scalar registers before any read
+                        uint64_t word[4];
+                        uint32_t below[4];   // new keys before each chunk
+#pragma unroll
+                        for (uint32_t u = 0; u < 4; ++u) {
+                            word[u] = u < ng ? readlane64(pwl, (int)(g - 1u - u - w_lo)) : 0ull;
+                            above += (uint32_t)__popcll(word[u]);
+                            below[u] = n_placed - above;
+                        }
+                        uint64_t val[4];
+#pragma unroll
+                        for (uint32_t u = 0; u < 4; ++u) {
+                            const uint32_t o = ((g - 1u - u) << 6) + lane;
+                            const bool isnew = (word[u] >> lane) & 1ull;
+                            const uint32_t cnt = below[u] + (uint32_t)__popcll(word[u] & ((1ull << lane) - 1ull));
+                            val[u] = 0;
+                            if (u < ng && o >= p0 && o < newlen) val[u] = isnew ? nkey[cnt] : beam[o - cnt];
                         }
                         wave_sync();
+#pragma unroll
+                        for (uint32_t u = 0; u < 4; ++u) {
+                            const uint32_t o = ((g - 1u - u) << 6) + lane;
+                            if (u < ng && o >= p0 && o < newlen) beam[o] = val[u];
+                        }
+                        wave_sync();
+                        g -= ng;
                     }
                     len = newlen;
                     if (p0 < scan_from) scan_from = p0;
@@ -926,6 +1047,18 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             PROF_T(t_row);
             PROF_ADD(12, t_row - t_sel1);
 
+            // row-gather scorers: every neighbour's attribute record and
+            // vector requested now, so that the gathers overlap the visited
+            // test; only the new neighbours' keys are entered (the same
+            // candidates, distances and keys as scoring after the test)
+            typename Scorer::RowGather rg;
+            int4 aw0 = make_int4(0, 0, 0, 0), aw1 = make_int4(0, 0, 0, 0);
+            if constexpr (Scorer::kSpec) {
+                const uint32_t vv = v != BOA_PAD ? v : ix.entry;   // padding: any valid row, unused
+                if (lane < R) load_attrs(vv, aw0, aw1);
+                sc.gather_row(ix.vectors, d, vv, R, lane, rg);
+            }
+
             // ---- test-and-insert into the visited set
             const int vst = visit_test(v);
             PROF_T(t_vl);
@@ -934,19 +1067,35 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             const uint64_t nm = __ballot(is_new);
             c = __popcll(nm);
             PROF_ADD(14, c == 0 ? 1 : 0);
-            if (is_new) cid[lanes_below(nm)] = v;
+            if (!Scorer::kSpec && is_new) cid[lanes_below(nm)] = v;
             // the row of the entry expected next is requested only now: a
             // load issued before the visited test would be waited for there
-            // (loads retire in order), while from here it overlaps the gathers
+            // (loads retire in order), while from here it overlaps the gathers.
+            // It is requested on every path (the entry's row when nothing is
+            // predicted), so that waiting for the gathers is one fixed count.
             pf_key = kn;
-            pf_id = BOA_PAD;
-            if (j2 >= 0) {
-                pf_id = key_id(kn);
-                pf_row = lane < R ? ix.adj[(size_t)pf_id * R + lane] : BOA_PAD;
+            {
+                // (every lane loads, lanes past R from the row's last slot:
+                // a load under a branch would leave the count unknown)
+                const uint32_t pid = j2 >= 0 ? key_id(kn) : ix.entry;
+                pf_id = j2 >= 0 ? pid : BOA_PAD;
+                const uint32_t pr = ix.adj[(size_t)pid * R + (lane < R ? lane : R - 1)];
+                pf_row = lane < R ? pr : BOA_PAD;
             }
             PROF_T(t_vis1);
             PROF_ADD(1, t_vis1 - t_sel1);
             PROF_ADD(6, spill ? 1 : 0);
+            if constexpr (Scorer::kSpec) {
+                // the gathered neighbours' distances, then the new ones' keys
+                const uint32_t phi = count_phi(aw0, aw1);
+                sc.score_row(rg, d, R, cd, lane);
+                wave_sync();
+                spec_key = is_new ? make_key(phi, cd[lane], v) : KEY_NONE;
+                spec_c = c;
+                c = 0;
+                PROF_T(t_spec1);
+                PROF_ADD(2, t_spec1 - t_vis1);
+            }
         }
 
         // ---- epilogue: confidence (Eq. 3) over the phase's worklist (its
@@ -1034,6 +1183,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         if (last) break;
         }   // phases
     }       // queries
+    if (!a.vis_bitmap && lane == 0) vs.log[0] = n_log;
 #ifdef BOA_STAGE_PROFILE
     if (lane == 0 && a.prof) {
         for (int i = 0; i < BOA_PROF_SLOTS; ++i) a.prof[(size_t)slot * BOA_PROF_SLOTS + i] += prof_acc[i];
@@ -1112,6 +1262,7 @@ __global__ void init_kernel(InitArgs a)
     }
     if (a.qstat && i < (size_t)a.nq * a.n_phases) a.qstat[i] = 0;
     if (i < (size_t)a.n_counters) a.counters[i] = 0;
+    if (i < a.reset_slots) a.bits[i * a.slot_words + a.bits_words] = BOA_LOG_DIRTY;
     if (i == 0) {
         a.n_active[0] = (uint32_t)a.nq;
         // later phases' counts and the BOA+ pool counts
@@ -1227,6 +1378,7 @@ hipError_t launch_init(const InitArgs &a, hipStream_t st)
 {
     size_t n = (size_t)a.nq * (a.n_phases > 1 ? a.n_phases : 1);
     if ((size_t)a.n_counters > n) n = a.n_counters;
+    if (a.reset_slots > n) n = (size_t)a.reset_slots;
     if (n == 0) n = 1;
     unsigned blocks = (unsigned)((n + 255) / 256);
     hipLaunchKernelGGL(init_kernel, dim3(blocks), dim3(256), 0, st, a);
