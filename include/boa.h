@@ -138,7 +138,7 @@ typedef struct {
     int32_t sub_batches;    /* BOA+ first-phase sub-batches; default 10 */
     int32_t lds_hash_slots; /* 0: automatic; else a power of two in [64, 16384] that forces
                                the 16-bit slots of the per-wave LDS visited table (tests
-                               force spills to the HBM bitmap); at least 8 * 2^(B-14)
+                               force spills to the HBM bitmap); at least 8 * 2^(B-15)
                                for ids of B bits */
     const int32_t *schedule; /* optional host array of explicit phase widths
                                 (strictly increasing); overrides L0/Lmax/alpha */

@@ -471,11 +471,11 @@ uint32_t id_bits(const boa_index *ix)
     return b;
 }
 
-// 8 slots per bucket, at most 14 stored bits per id
+// 8 slots per bucket, at most 15 stored bits per id
 uint32_t min_table_slots(const boa_index *ix)
 {
     const uint32_t B = id_bits(ix);
-    return std::max<uint32_t>(64u, B > 14 ? (8u << (B - 14)) : 64u);
+    return std::max<uint32_t>(64u, B > 15 ? (8u << (B - 15)) : 64u);
 }
 
 PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t max_active, bool wide = false,
@@ -486,7 +486,7 @@ PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t m
     pl.wide = wide;
     // visited table: 16-bit slots, 16 per expected scored node of a width-L
     // search, between 1024 and 4096 (2-8 KB); ids that find both of their
-    // buckets full go to the HBM bitmap. The table must leave at most 14
+    // buckets full go to the HBM bitmap. The table must leave at most 15
     // stored bits per id.
     uint32_t h = forced_h > 0 ? (uint32_t)forced_h
                               : std::min<uint32_t>(4096u, std::max<uint32_t>(1024u, next_pow2(16ull * L)));

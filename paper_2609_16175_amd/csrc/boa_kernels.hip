@@ -142,6 +142,7 @@ struct F32Scorer {
     // lane p = lane & 15 accumulates float4 chunks p, p+16, p+32, ...
     static constexpr bool kWide = W == 2;
     static constexpr bool kSpec = false;
+    static constexpr int kSpecMaxR = 0;
     struct RowGather {};
     __device__ __forceinline__ void gather_row(const void *, int, uint32_t, int, int, RowGather &) const {}
     __device__ __forceinline__ void score_row(const RowGather &, int, int, float *, int) const {}
@@ -297,7 +298,9 @@ struct U8Scorer {
     }
 
     static constexpr int PER = 64 / G;   // candidates per round
-    static constexpr int RU = W == 1 ? (G <= 8 ? 2 : 4) : (G <= 16 ? G : 16);
+    // rows in flight per round trip of score(); with row gathers it scores
+    // only the entry point and rows longer than the gathers cover
+    static constexpr int RU = (W == 1 || G <= 8) ? (G <= 8 ? 2 : 4) : (G <= 16 ? G : 16);
     struct Ids {
         uint32_t v[RU];
     };
@@ -343,7 +346,9 @@ struct U8Scorer {
     // holds row entry j (padding replaced by a valid id), and round u's
     // G-lane group g loads chunk p of entry PER u + g. All rounds' loads are
     // issued together; score_row waits for them.
-    static constexpr int RS = kSpec ? (BOA_MAX_R + PER - 1) / PER : 1;
+    static constexpr int RS_ALL = (BOA_MAX_R + PER - 1) / PER;
+    static constexpr int RS = !kSpec ? 1 : (RS_ALL < 4 ? RS_ALL : 4);
+    static constexpr int kSpecMaxR = kSpec ? PER * RS : 0;   // longer rows take the other path
     struct RowGather {
         uint4 x[RS];
     };
@@ -382,7 +387,9 @@ struct U8Scorer {
     // chunk p in x); the group's top lane returns it
     __device__ __forceinline__ int32_t dist(uint4 x, int p, int nch) const
     {
-        if (p >= nch) x = q;   // lanes past the row: add zero
+        if (nch < G) {         // (uniform) lanes past the row add zero
+            if (p >= nch) x = q;
+        }
         int32_t acc = (int32_t)(dot16(x, x) + qq - 2u * dot16(x, q));
         // exact integer sum over the group; the group's top lane holds it
 #pragma unroll
@@ -404,6 +411,7 @@ template <int T>
 struct PQScorer {
     static constexpr bool kWide = false;
     static constexpr bool kSpec = false;
+    static constexpr int kSpecMaxR = 0;
     struct RowGather {};
     __device__ __forceinline__ void gather_row(const void *, int, uint32_t, int, int, RowGather &) const {}
     __device__ __forceinline__ void score_row(const RowGather &, int, int, float *, int) const {}
@@ -564,10 +572,11 @@ __device__ __forceinline__ uint64_t wave_min64(uint64_t v)
 // ---------------------------------------------------------------------------
 // Visited set (exact). LDS part: a two-choice bucketed table of 16-bit
 // entries. A bijective mix of the id's B bits gives h; its top bits select
-// the home bucket b1, the low r = B - log2(buckets) <= 14 bits are stored.
+// the home bucket b1, the low r = B - log2(buckets) <= 15 bits are stored.
 // The alternate bucket is b2 = b1 ^ alt(r) (alt odd, so b2 != b1). An entry
-// is 0x8000 | r in b1 or 0xC000 | r in b2, so (bucket, entry) identifies the
-// id uniquely. A bucket holds 8 entries (16 bytes, one LDS read).
+// is r in b1 or 0x8000 | r in b2, so (bucket, entry) identifies the id
+// uniquely; 0xFFFF marks a free slot, so an id whose r is 0x7FFF has no
+// alternate bucket. A bucket holds 8 entries (16 bytes, one LDS read).
 // Insert goes to the emptier bucket through a 32-bit CAS on the word that
 // holds the slot. When both buckets are full the id goes to the wave slot's
 // bitmap over all points in HBM (cleared when a query first overflows).
@@ -592,12 +601,14 @@ struct Visited {
     uint32_t *status;
 };
 
+// ids have at most 24 bits (BOA_MAX_N), so 24-bit multiplies (full rate)
+// by odd constants are bijections modulo 2^B
 __device__ __forceinline__ uint32_t mix_id(uint32_t v, uint32_t B)
 {
-    const uint32_t mask = B >= 32 ? 0xFFFFFFFFu : ((1u << B) - 1u);
-    uint32_t h = (v * 0x9E3779B1u) & mask;
+    const uint32_t mask = (1u << B) - 1u;
+    uint32_t h = __umul24(v, 0x3779B1u) & mask;
     h ^= h >> ((B + 1u) >> 1);
-    return (h * 0x85EBCA6Bu) & mask;
+    return __umul24(h, 0xEBCA6Bu) & mask;
 }
 
 // Bit 15 of each 16-bit half of the result is set when that half of w is
@@ -615,10 +626,11 @@ __device__ __forceinline__ bool has16(const uint4 &b, uint32_t e)
     return (zero_halves(b.x ^ ee) | zero_halves(b.y ^ ee) | zero_halves(b.z ^ ee) | zero_halves(b.w ^ ee)) != 0u;
 }
 
+// free slots (0xFFFF halves) of a bucket
 __device__ __forceinline__ uint32_t empties16(const uint4 &b)
 {
-    return (uint32_t)__popc(zero_halves(b.x) | (zero_halves(b.y) >> 1) | (zero_halves(b.z) >> 2) |
-                            (zero_halves(b.w) >> 3));
+    return (uint32_t)__popc(zero_halves(~b.x) | (zero_halves(~b.y) >> 1) | (zero_halves(~b.z) >> 2) |
+                            (zero_halves(~b.w) >> 3));
 }
 
 // 1: v was not in the set and now is (in LDS); 0: v was already there;
@@ -628,14 +640,15 @@ __device__ __forceinline__ int visit_lds(const Visited &s, uint32_t v)
     const uint32_t h = mix_id(v, s.idbits);
     const uint32_t r = h & ((1u << s.rbits) - 1u);
     const uint32_t b1 = h >> s.rbits;
-    const uint32_t b2 = (b1 ^ (((r * 0x5BD1E995u + 0x7F4A7C15u) >> 7) | 1u)) & s.bmask;
-    const uint32_t e1 = 0x8000u | r, e2 = 0xC000u | r;
+    const uint32_t b2 = (b1 ^ (((__umul24(r, 0xD1E995u) + 0x7F4A7C15u) >> 7) | 1u)) & s.bmask;
+    const uint32_t e1 = r, e2 = 0x8000u | r;
+    const bool alt_ok = e2 != 0xFFFFu;
     const uint4 *bk = reinterpret_cast<const uint4 *>(s.words);
     for (int attempt = 0; attempt < 256; ++attempt) {
         // both buckets read before either is tested: one LDS round trip
         const uint4 B1 = bk[b1], B2 = bk[b2];
-        if (has16(B1, e1) | has16(B2, e2)) return 0;
-        const uint32_t n1 = empties16(B1), n2 = empties16(B2);
+        if (has16(B1, e1) | (alt_ok && has16(B2, e2))) return 0;
+        const uint32_t n1 = empties16(B1), n2 = alt_ok ? empties16(B2) : 0u;
         if (n1 == 0u && n2 == 0u) return -1;
         const bool use1 = n1 >= n2;
         const uint4 Bc = use1 ? B1 : B2;
@@ -647,11 +660,11 @@ __device__ __forceinline__ int visit_lds(const Visited &s, uint32_t v)
         uint32_t wi = 0, old = 0, neu = 0;
 #pragma unroll
         for (int q = 3; q >= 0; --q) {
-            const uint32_t zq = zero_halves(w[q]);
+            const uint32_t zq = zero_halves(~w[q]);
             if (zq) {
                 wi = q;
                 old = w[q];
-                neu = w[q] | ((zq & 0x8000u) ? e : (e << 16));
+                neu = (zq & 0x8000u) ? ((w[q] & 0xFFFF0000u) | e) : ((w[q] & 0x0000FFFFu) | (e << 16));
             }
         }
         if (atomicCAS(&s.words[bi * 4u + wi], old, neu) == old) return 1;
@@ -720,6 +733,8 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
 
     const IndexView ix = a.ix;
     const int R = ix.R, d = ix.d, m = ix.m;
+    // row gathers ahead of the visited test (scorers that have them, rows they cover)
+    const bool spec = Scorer::kSpec && R <= Scorer::kSpecMaxR;
 
     const uint32_t n_in = bcast0(*a.n_active);
     if (n_in <= a.tau_count) return;   // the loop of Alg. 1 has stopped
@@ -805,7 +820,9 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         const int Lcap = (a.warm && p + 1 < a.p_end) ? a.sched[p + 1] : L;
         const bool fresh = !a.warm || p == a.p_begin;
         if (fresh) {
-            uint4 z = make_uint4(0, 0, 0, 0);
+            // the bitmap starts with no bit set, the table with every slot free
+            const uint32_t f = a.vis_bitmap ? 0u : 0xFFFFFFFFu;
+            const uint4 z = make_uint4(f, f, f, f);
             uint4 *h4 = reinterpret_cast<uint4 *>(htab);
             for (uint32_t i = lane; i < table_words >> 2; i += 64) h4[i] = z;
             spill = false;
@@ -1053,7 +1070,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             // candidates, distances and keys as scoring after the test)
             typename Scorer::RowGather rg;
             int4 aw0 = make_int4(0, 0, 0, 0), aw1 = make_int4(0, 0, 0, 0);
-            if constexpr (Scorer::kSpec) {
+            if (spec) {
                 const uint32_t vv = v != BOA_PAD ? v : ix.entry;   // padding: any valid row, unused
                 if (lane < R) load_attrs(vv, aw0, aw1);
                 sc.gather_row(ix.vectors, d, vv, R, lane, rg);
@@ -1067,7 +1084,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             const uint64_t nm = __ballot(is_new);
             c = __popcll(nm);
             PROF_ADD(14, c == 0 ? 1 : 0);
-            if (!Scorer::kSpec && is_new) cid[lanes_below(nm)] = v;
+            if (!spec && is_new) cid[lanes_below(nm)] = v;
             // the row of the entry expected next is requested only now: a
             // load issued before the visited test would be waited for there
             // (loads retire in order), while from here it overlaps the gathers.
@@ -1085,7 +1102,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             PROF_T(t_vis1);
             PROF_ADD(1, t_vis1 - t_sel1);
             PROF_ADD(6, spill ? 1 : 0);
-            if constexpr (Scorer::kSpec) {
+            if (spec) {
                 // the gathered neighbours' distances, then the new ones' keys
                 const uint32_t phi = count_phi(aw0, aw1);
                 sc.score_row(rg, d, R, cd, lane);

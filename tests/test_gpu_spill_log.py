@@ -90,3 +90,47 @@ def test_spill_log_fixed_widths(big):
         for slots in (128, 4096):
             got = gpu_search(big["gpu"], q, r, k=10, fixed_L=L, lds_hash_slots=slots)
             assert_parity(got, ref, f"fixed L={L} table {slots}")
+
+
+def _table_hash(v, B):
+    """The visited table's id mix (a bijection on B <= 24 bits), for
+    building inputs: two multiplications by odd 24-bit constants around an
+    xor-shift."""
+    mask = np.uint64((1 << B) - 1)
+    h = (v.astype(np.uint64) * np.uint64(0x3779B1)) & mask
+    h ^= h >> np.uint64((B + 1) >> 1)
+    return (h * np.uint64(0xEBCA6B)) & mask
+
+
+def test_ids_without_an_alternate_bucket():
+    """Ids of B = 19 bits in a 128-slot table keep 15 bits, and those whose
+    15 bits are all ones have no alternate bucket (that entry would read as
+    a free slot). The entry's row and theirs link them to each other, so
+    each is entered early, met again and, once its bucket fills, spilled;
+    results must equal the oracle's."""
+    import paper_2609_16175_amd as boa
+    n, d, m, R = 300_000, 16, 1, 12
+    hv = _table_hash(np.arange(n, dtype=np.uint64), 19)
+    special = np.flatnonzero((hv & np.uint64(0x7FFF)) == np.uint64(0x7FFF)).astype(np.uint32)
+    assert len(special) >= 4
+    adj = random_graph(n, R, 91)
+    entry = int(special[0])
+    for i, s in enumerate(special):
+        others = np.roll(special, -i)[1:R]
+        row = adj[s]
+        row[len(others):][np.isin(row[len(others):], special)] = PAD   # no repeats in the row
+        row[:len(others)] = others
+    rng = np.random.default_rng(91)
+    x = rng.integers(0, 256, size=(n, d)).astype(np.uint8)
+    a = rng.integers(0, 100, size=(n, m)).astype(np.int32)
+    t = np.zeros(m, dtype=np.int32)
+    orc = oracle.Index(x, a, t, adj, entry)
+    gpu = boa.Index(x, a, t, adj, entry)
+    q, r = random_queries(orc, 64, 70, seed=92)
+    for L in (16, 200):
+        ref = oracle.boa(orc, q, r, 10, [L])
+        for slots in (128, 256):
+            for kw in ({}, {"fused": True}):
+                got = gpu_search(gpu, q, r, k=10, fixed_L=L, lds_hash_slots=slots, **kw)
+                assert_parity(got, ref, f"special ids L={L} table {slots} {kw}")
+    gpu.close()
