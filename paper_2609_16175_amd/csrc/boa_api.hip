@@ -492,7 +492,7 @@ PhasePlan plan_phase(const boa_index *ix, int32_t L, int32_t forced_h, int64_t m
                               : std::min<uint32_t>(4096u, std::max<uint32_t>(1024u, next_pow2(16ull * L)));
     h = std::max<uint32_t>(h, min_table_slots(ix));
     pl.h_slots = (int32_t)h;
-    const int32_t Lb = (L + 1) & ~1, pw = ((L >> 6) + 3) & ~1;
+    const int32_t Lb = beam_slots(L), pw = ((L >> 6) + 3) & ~1;
     // (a product-quantised search also keeps its re-rank keys, Lb of them)
     pl.lds_per_wave = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 +
                       scorer_lds_bytes(ix->vec_dtype, ix->view.d, wide, pq_m) + (pq_m ? 8 * Lb : 0) + 2 * (int32_t)h;
@@ -579,7 +579,7 @@ PhasePlan plan_bitmap(const boa_index *ix, int32_t L, int64_t S, int pq_m = 0)
     pl.vis_bitmap = 1;
     pl.h_slots = 0;
     const int64_t words = ((ix->view.n + 31) / 32 + 3) & ~(int64_t)3;
-    const int32_t Lb = (L + 1) & ~1, pw = ((L >> 6) + 3) & ~1;
+    const int32_t Lb = beam_slots(L), pw = ((L >> 6) + 3) & ~1;
     const int64_t lds = 8 * Lb + 8 * 64 + 8 * pw + 4 * 64 + 4 * 64 + scorer_lds_bytes(ix->vec_dtype, ix->view.d, true, pq_m) +
                         (pq_m ? 8 * Lb : 0) + 4 * words;
     pl.lds_per_wave = (int32_t)((lds + 15) & ~(int64_t)15);

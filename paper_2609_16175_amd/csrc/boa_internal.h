@@ -17,6 +17,16 @@
 
 namespace boa {
 
+// Worklist slots of a wave: a power of two at least L (entries past the
+// list's length hold the largest key, so a search for an insertion point
+// runs over a power-of-two span without bounds checks).
+__host__ __device__ inline int32_t beam_slots(int32_t L)
+{
+    int32_t p = 2;
+    while (p < L) p <<= 1;
+    return p;
+}
+
 // Device-resident index. Attribute rows are padded to m_pad in {1, 2, 4, 8}
 // cells so one aligned vector load fetches a whole record.
 struct IndexView {

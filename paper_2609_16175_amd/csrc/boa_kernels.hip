@@ -94,27 +94,27 @@ __device__ __forceinline__ uint32_t lower_bound64(const uint64_t *a, uint32_t n,
     }
     return lo;
 }
-// the same index by an eight-way search: seven independent LDS reads per
-// step, so a lone wave waits for a third as many round trips (512 entries:
-// three steps instead of nine)
-__device__ __forceinline__ uint32_t lower_bound64_8way(const uint64_t *a, uint32_t n, uint64_t key)
+// The same index in a[0, P) for a power of two P whose entries from n on
+// hold KEY_NONE (greater than any key), by eight-way steps: seven
+// independent LDS reads per step at shifted offsets, the same number of
+// steps in every lane (512 entries: three eight-way steps and one compare).
+// The answer stays in [b, b + s]; pivot j of a step (stride s / 8) is below
+// the key exactly when at least j s / 8 entries from b are.
+__device__ __forceinline__ uint32_t lower_bound64_p2(const uint64_t *a, uint32_t P, uint64_t key)
 {
-    uint32_t lo = 0, hi = n;   // the answer lies in [lo, hi]
-    while (hi - lo > 7u) {
-        const uint32_t q = (hi - lo) >> 3;
-        uint32_t below = 0;    // pivots lo + i q (i = 1..7) holding a key < key
+    uint32_t b = 0, sh = 31u - (uint32_t)__clz(P);   // s = 2^sh = P
+    while (sh >= 3u) {   // uniform
+        sh -= 3u;
+        uint32_t below = 0;
 #pragma unroll
-        for (uint32_t i = 1; i <= 7; ++i) below += a[lo + i * q] < key ? 1u : 0u;
-        // keys are sorted, so the pivots below key are the first `below` ones
-        const uint32_t nlo = below == 0u ? lo : lo + below * q + 1u;
-        hi = below == 7u ? hi : lo + (below + 1u) * q;
-        lo = nlo;
+        for (uint32_t j = 1; j <= 7; ++j) below += a[b + (j << sh) - 1u] < key ? 1u : 0u;
+        b += below << sh;
     }
-    while (lo < hi) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (a[mid] < key) lo = mid + 1u; else hi = mid;
+    while (sh > 0u) {    // s in {2, 4}: halve
+        sh -= 1u;
+        if (a[b + (1u << sh) - 1u] < key) b += 1u << sh;
     }
-    return lo;
+    return b + (a[b] < key ? 1u : 0u);
 }
 
 // Cross-lane move inside a 16-lane row by DPP (no LDS round trip):
@@ -719,7 +719,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     // ids and distances, visited table; sized for the widest phase of the launch
     unsigned char *mine = smem + (size_t)wid * a.lds_per_wave;
     // (sizes keep every array 16-byte aligned: Lb and the bitmap word count are even)
-    const int Lb = (a.L_alloc + 1) & ~1;
+    const int Lb = beam_slots(a.L_alloc);
     const int pw = ((a.L_alloc >> 6) + 3) & ~1;
     uint64_t *beam = reinterpret_cast<uint64_t *>(mine);         // Lb
     uint64_t *nkey = beam + Lb;                                  // 64
@@ -820,11 +820,13 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         const int Lcap = (a.warm && p + 1 < a.p_end) ? a.sched[p + 1] : L;
         const bool fresh = !a.warm || p == a.p_begin;
         if (fresh) {
-            // the bitmap starts with no bit set, the table with every slot free
+            // the bitmap starts with no bit set, the table with every slot
+            // free, the worklist with every slot past its (zero) length KEY_NONE
             const uint32_t f = a.vis_bitmap ? 0u : 0xFFFFFFFFu;
             const uint4 z = make_uint4(f, f, f, f);
             uint4 *h4 = reinterpret_cast<uint4 *>(htab);
             for (uint32_t i = lane; i < table_words >> 2; i += 64) h4[i] = z;
+            for (int i = lane; i < Lb; i += 64) beam[i] = KEY_NONE;
             spill = false;
             len = 0;
         }
@@ -957,7 +959,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                     uint32_t f = 0xFFFFFFFFu;
                     uint32_t pos = 0;
                     if (lane < (int)kept) {
-                        pos = Scorer::kWide ? lower_bound64_8way(beam, len, key) : lower_bound64(beam, len, key);
+                        pos = lower_bound64_p2(beam, (uint32_t)beam_slots((int32_t)len), key);
                         f = pos + lane;
                     }
                     const uint32_t p0 = bcast0(pos);
