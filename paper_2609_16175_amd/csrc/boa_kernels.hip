@@ -949,7 +949,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                         if (k0 < pf_key) {
                             pf_key = k0;
                             pf_id = key_id(k0);
-                            pf_row = lane < R ? ix.adj[(size_t)pf_id * R + lane] : BOA_PAD;
+                            pf_row = ix.adj[(size_t)pf_id * R + (lane < R ? lane : R - 1)];
                             PROF_ADD(9, 1);
                         }
                     }
@@ -975,42 +975,23 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
                     PROF_T(t_rank1);
                     PROF_ADD(4, t_rank1 - t_sort1);
                     PROF_ADD(7, w_hi - w_lo + 1);
-                    // rebuild [p0, newlen) from the last 64-slot chunk down, four
-                    // chunks at a time: their reads first (independent), then
-                    // their writes. An entry moves only upwards, so a group's
-                    // writes land above every source of the groups after it.
-                    // Lane i holds chunk w_lo + i's bitmap word (at most 33
-                    // chunks for a width of 2048).
-                    const uint64_t pwl = lane <= (int)(w_hi - w_lo) ? posbm[w_lo + lane] : 0ull;
-                    uint32_t above = 0;   // new keys in the chunks already done
-                    for (uint32_t g = w_hi + 1u; g > w_lo;) {   // g: one past the group's top chunk
-                        const uint32_t ng = min(4u, g - w_lo);
-                        // the group's bitmap words, into scalar registers before any read
-                        uint64_t word[4];
-                        uint32_t below[4];   // new keys before each chunk
-#pragma unroll
-                        for (uint32_t u = 0; u < 4; ++u) {
-                            word[u] = u < ng ? readlane64(pwl, (int)(g - 1u - u - w_lo)) : 0ull;
-                            above += (uint32_t)__popcll(word[u]);
-                            below[u] = n_placed - above;
-                        }
-                        uint64_t val[4];
-#pragma unroll
-                        for (uint32_t u = 0; u < 4; ++u) {
-                            const uint32_t o = ((g - 1u - u) << 6) + lane;
-                            const bool isnew = (word[u] >> lane) & 1ull;
-                            const uint32_t cnt = below[u] + (uint32_t)__popcll(word[u] & ((1ull << lane) - 1ull));
-                            val[u] = 0;
-                            if (u < ng && o >= p0 && o < newlen) val[u] = isnew ? nkey[cnt] : beam[o - cnt];
+                    // rebuild [p0, newlen) from the last 64-slot chunk down
+                    uint64_t word = posbm[w_hi];
+                    uint32_t below = n_placed - (uint32_t)__popcll(word);   // new keys before chunk
+                    for (int w = (int)w_hi; w >= (int)w_lo; --w) {
+                        const uint32_t o = ((uint32_t)w << 6) + lane;
+                        const bool act = o >= p0 && o < newlen;
+                        const bool isnew = (word >> lane) & 1ull;
+                        const uint32_t cnt = below + (uint32_t)__popcll(word & ((1ull << lane) - 1ull));
+                        uint64_t val = 0;
+                        if (act) val = isnew ? nkey[cnt] : beam[o - cnt];
+                        wave_sync();
+                        if (act) beam[o] = val;
+                        if (w > (int)w_lo) {
+                            word = posbm[w - 1];
+                            below -= (uint32_t)__popcll(word);
                         }
                         wave_sync();
-#pragma unroll
-                        for (uint32_t u = 0; u < 4; ++u) {
-                            const uint32_t o = ((g - 1u - u) << 6) + lane;
-                            if (u < ng && o >= p0 && o < newlen) beam[o] = val[u];
-                        }
-                        wave_sync();
-                        g -= ng;
                     }
                     len = newlen;
                     if (p0 < scan_from) scan_from = p0;
@@ -1054,7 +1035,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             // ---- adjacency row (prefetched if predicted)
             uint32_t v;
             if (u == pf_id) {
-                v = pf_row;
+                v = lane < R ? pf_row : BOA_PAD;
                 PROF_ADD(8, 1);
             } else {
                 v = lane < R ? ix.adj[(size_t)u * R + lane] : BOA_PAD;
@@ -1095,11 +1076,12 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             pf_key = kn;
             {
                 // (every lane loads, lanes past R from the row's last slot:
-                // a load under a branch would leave the count unknown)
+                // a load under a branch would leave the count unknown; the
+                // row is masked where it is used, since a select here would
+                // wait for the load at once)
                 const uint32_t pid = j2 >= 0 ? key_id(kn) : ix.entry;
                 pf_id = j2 >= 0 ? pid : BOA_PAD;
-                const uint32_t pr = ix.adj[(size_t)pid * R + (lane < R ? lane : R - 1)];
-                pf_row = lane < R ? pr : BOA_PAD;
+                pf_row = ix.adj[(size_t)pid * R + (lane < R ? lane : R - 1)];
             }
             PROF_T(t_vis1);
             PROF_ADD(1, t_vis1 - t_sel1);
