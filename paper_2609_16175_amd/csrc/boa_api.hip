@@ -282,17 +282,24 @@ int boa_build_index_ex(const void *vectors, int64_t n, int32_t d, int32_t vec_dt
         boa_free_index(ix);
         return rc;
     }
+    // the search's copy of the attributes: rows padded to m_pad cells, float32
+    // columns as order-preserving integers, so that every range test is an
+    // integer compare (the caller's array is not modified)
     std::vector<int32_t> padded;
     const int32_t *attr_src = attrs;
-    if (m_pad != m) {
+    if (m_pad != m || f32_mask != 0) {
         try {
             padded.assign((size_t)n * m_pad, 0);
         } catch (...) {
             boa_free_index(ix);
             return fail(BOA_ENOMEM, "host allocation failed");
         }
-        for (int64_t i = 0; i < n; ++i)
-            std::memcpy(&padded[(size_t)i * m_pad], attrs + (size_t)i * m, sizeof(int32_t) * m);
+        for (int64_t i = 0; i < n; ++i) {
+            int32_t *dst = &padded[(size_t)i * m_pad];
+            const int32_t *src = attrs + (size_t)i * m;
+            for (int j = 0; j < m; ++j)
+                dst[j] = ((f32_mask >> j) & 1u) ? f32_ord((uint32_t)src[j]) : src[j];
+        }
         attr_src = padded.data();
     }
     if (hipMemcpy(ix->d_vectors, vectors, (size_t)n * d * esz, hipMemcpyHostToDevice) != hipSuccess ||

@@ -27,11 +27,23 @@ __host__ __device__ inline int32_t beam_slots(int32_t L)
     return p;
 }
 
+// A float32 attribute cell as an order-preserving int32: for floats a, b
+// that are not NaN, a <= b exactly when f32_ord(a) <= f32_ord(b) (both zeros
+// map to 0, so -0 and +0 compare equal as floats do). NaN maps to INT32_MIN,
+// below the image of every other value (-inf maps to -2^31 + 2^23 - 1).
+__host__ __device__ inline int32_t f32_ord(uint32_t x)
+{
+    const uint32_t mag = x & 0x7FFFFFFFu;
+    if (mag == 0u) return 0;
+    if (mag > 0x7F800000u) return (int32_t)0x80000000u;
+    return (int32_t)(x ^ ((uint32_t)((int32_t)x >> 31) & 0x7FFFFFFFu));
+}
+
 // Device-resident index. Attribute rows are padded to m_pad in {1, 2, 4, 8}
 // cells so one aligned vector load fetches a whole record.
 struct IndexView {
     const void *vectors;      // n x d (float32 or uint8)
-    const int32_t *attrs;     // n x m_pad cells
+    const int32_t *attrs;     // n x m_pad cells; float32 columns as f32_ord
     const uint32_t *adj;      // n x R
     int64_t n;
     int32_t d, m, m_pad, R;

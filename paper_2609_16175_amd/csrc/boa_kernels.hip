@@ -32,6 +32,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "boa_internal.h"
 
 namespace boa {
@@ -772,24 +774,31 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
             w0.x = ar[0];
         }
     };
-    int32_t lo[BOA_MAX_M], hi[BOA_MAX_M];
+    // Eq. 2's phi: the number of violated predicates. The index holds float32
+    // cells as order-preserving integers, and each query's bounds are mapped
+    // the same way, so a cell satisfies its range [lo, hi] exactly when
+    // (uint32)(x - lo) <= hi - lo. A range that nothing satisfies (lo > hi, or
+    // a NaN bound of a float32 column, which fails every comparison) counts
+    // in phi0 for every point; its cell, like a padding cell, then passes.
+    int32_t flo[BOA_MAX_M];
+    uint32_t fspan[BOA_MAX_M];
+    uint32_t phi0 = 0;
     auto count_phi = [&](const int4 &w0, const int4 &w1) -> uint32_t {
         const int32_t av[BOA_MAX_M] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-        uint32_t phi = 0;
+        // the record's m_pad cells (one uniform dispatch, no per-cell tests)
+        auto cells = [&](auto nc_tag) -> uint32_t {
+            constexpr int NC = decltype(nc_tag)::value;
+            uint32_t phi = phi0;
 #pragma unroll
-        for (int j = 0; j < BOA_MAX_M; ++j) {
-            if (j < m) {
-                bool ok;
-                if ((ix.f32_mask >> j) & 1u) {
-                    const float x = __int_as_float(av[j]);
-                    ok = (__int_as_float(lo[j]) <= x) && (x <= __int_as_float(hi[j]));
-                } else {
-                    ok = (lo[j] <= av[j]) && (av[j] <= hi[j]);
-                }
-                phi += ok ? 0u : 1u;
-            }
+            for (int j = 0; j < NC; ++j) phi += (uint32_t)(av[j] - flo[j]) > fspan[j] ? 1u : 0u;
+            return phi;
+        };
+        switch (ix.m_pad) {
+        case 1: return cells(std::integral_constant<int, 1>{});
+        case 2: return cells(std::integral_constant<int, 2>{});
+        case 4: return cells(std::integral_constant<int, 4>{});
+        default: return cells(std::integral_constant<int, 8>{});
         }
-        return phi;
     };
 #ifdef BOA_STAGE_PROFILE
     uint64_t prof_acc[BOA_PROF_SLOTS] = {};
@@ -802,10 +811,32 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         const uint32_t qi = bcast0(a.active[t]);
 
         sc.load_query(a.queries, qi, d, lane);
+        phi0 = 0;
 #pragma unroll
         for (int j = 0; j < BOA_MAX_M; ++j) {
-            lo[j] = j < m ? a.ranges[((size_t)qi * m + j) * 2 + 0] : 0;
-            hi[j] = j < m ? a.ranges[((size_t)qi * m + j) * 2 + 1] : 0;
+            int32_t l = 0;
+            uint32_t s = 0xFFFFFFFFu;   // (padding cells pass)
+            if (j < m) {
+                int32_t lo = a.ranges[((size_t)qi * m + j) * 2 + 0];
+                int32_t hi = a.ranges[((size_t)qi * m + j) * 2 + 1];
+                bool none = false;
+                if ((ix.f32_mask >> j) & 1u) {
+                    none = ((uint32_t)lo & 0x7FFFFFFFu) > 0x7F800000u || ((uint32_t)hi & 0x7FFFFFFFu) > 0x7F800000u;
+                    lo = f32_ord((uint32_t)lo);
+                    hi = f32_ord((uint32_t)hi);
+                }
+                if (none || lo > hi) {
+                    phi0 += 1;
+                } else {
+                    l = lo;
+                    s = (uint32_t)hi - (uint32_t)lo;
+                }
+            }
+            // (held in vector registers: kept uniform they would be spilled
+            // scalars, reloaded at every use)
+            asm volatile("" : "+v"(l), "+v"(s));
+            flo[j] = l;
+            fspan[j] = s;
         }
         // the phases of this launch: each restarts the search from the entry
         // point at its own width (Alg. 1 calls Alg. 2 afresh)

@@ -257,6 +257,83 @@ def test_shapes(shape):
     gpu.close()
 
 
+# ---------------------------------------------------------------------------
+# attribute cells at the edges of their types: float32 zeros of both signs,
+# infinities, NaNs (either sign, quiet and signalling), denormals and
+# extremes; int32 extremes; bounds of the same kinds, NaN bounds and empty
+# ranges. The oracle compares each column in its own type.
+
+def _f32_cells(vals):
+    return np.asarray(vals, dtype=np.float32).view(np.int32)
+
+
+F32_EDGE_CELLS = np.concatenate([
+    _f32_cells([0.0, -0.0, np.inf, -np.inf, 1e-45, -1e-45, 1.1754944e-38, -1.1754944e-38,
+                3.4028235e38, -3.4028235e38, 1.0, -1.0, 0.5, -0.5]),
+    np.array([0x7FC00000, 0x7F800001, 0xFFC00000, 0xFFFFFFFF], dtype=np.uint32).view(np.int32),   # NaNs
+])
+I32_EDGE_CELLS = np.array([-2**31, -2**31 + 1, -1, 0, 1, 2**31 - 2, 2**31 - 1], dtype=np.int32)
+
+
+def _edge_case_inputs(dtype, d, R, seed):
+    """An index whose columns are (int32, float32, float32): a quarter of the
+    cells from the edge sets, the rest ordinary; and queries whose bounds mix
+    the same values with ordinary ones (empty and NaN-bounded ranges too)."""
+    x, attrs, _, adj, entry = random_arrays(n=3000, d=d, m=3, R=R, dtype=dtype, seed=seed)
+    rng = np.random.default_rng(seed + 7)
+    n = x.shape[0]
+    types = np.array([0, 1, 1], dtype=np.int32)
+    a = np.empty((n, 3), dtype=np.int32)
+    a[:, 0] = rng.integers(-50, 50, n)
+    a[:, 1] = _f32_cells(rng.normal(size=n))
+    a[:, 2] = _f32_cells(np.round(rng.normal(size=n), 1))   # many exact zeros, some -0.0
+    edge = rng.random((n, 3)) < 0.25
+    a[:, 0] = np.where(edge[:, 0], rng.choice(I32_EDGE_CELLS, n), a[:, 0])
+    a[:, 1] = np.where(edge[:, 1], rng.choice(F32_EDGE_CELLS, n), a[:, 1])
+    a[:, 2] = np.where(edge[:, 2], rng.choice(F32_EDGE_CELLS, n), a[:, 2])
+    orc = oracle.Index(x, a, types, adj, entry)
+    q, _ = random_queries(orc, 160, 40, seed=seed)
+    nq = q.shape[0]
+    r = np.empty((nq, 3, 2), dtype=np.int32)
+    lo0 = rng.integers(-70, -20, nq)
+    r[:, 0, 0], r[:, 0, 1] = lo0, lo0 + rng.integers(-5, 130, nq)          # a few lo > hi
+    ii = rng.random(nq) < 0.15
+    r[ii, 0, 0] = rng.choice(I32_EDGE_CELLS[:3], ii.sum())
+    r[ii, 0, 1] = rng.choice(I32_EDGE_CELLS[3:], ii.sum())
+    r[:, 1, 0], r[:, 1, 1] = _f32_cells(-2.5 + rng.random(nq)), _f32_cells(1.5 + rng.random(nq))
+    r[:, 2, 0], r[:, 2, 1] = _f32_cells(np.full(nq, -3.0)), _f32_cells(np.full(nq, 3.0))
+    for col in (1, 2):
+        for side in (0, 1):
+            jj = rng.random(nq) < 0.12
+            r[jj, col, side] = rng.choice(F32_EDGE_CELLS, jj.sum())
+    r[rng.random(nq) < 0.12, 2, :] = _f32_cells([-0.0, 0.0])      # only the zeros
+    r[rng.random(nq) < 0.12, 2, :] = _f32_cells([0.0, -0.0])
+    r[rng.random(nq) < 0.12, 2, :] = _f32_cells([-np.inf, np.inf])
+    return x, a, types, adj, entry, orc, q, r
+
+
+@pytest.mark.parametrize("dtype,d,R", [("u8", 128, 32), ("f32", 32, 16)])
+def test_attribute_edge_values(dtype, d, R):
+    boa = _boa()
+    x, a, types, adj, entry, orc, q, r = _edge_case_inputs(dtype, d, R, seed=d + R)
+    valid = np.array([[oracle.phi(a[i], r[t], types) == 0 for i in range(0, a.shape[0], 7)]
+                      for t in range(0, q.shape[0], 8)])
+    assert 0.0 < valid.mean() < 1.0 and (~valid.any(1)).any()   # both kinds of valid set occur
+    gpu = boa.Index(x, a, types, adj, entry)
+    sched = oracle.schedule(16, 2.0, 128)
+    ref = oracle.boa(orc, q, r, 10, sched, eps=0.1)
+    for kw in ({}, {"fused": True}, {"split": True}):
+        got = gpu_search(gpu, q, r, k=10, L0=16, Lmax=128, eps=0.1, **kw)
+        assert_parity(got, ref, f"edge values {dtype} {kw}")
+    ref_w = oracle.boa_warm(orc, q, r, 10, sched, eps=0.1)
+    got = gpu_search(gpu, q, r, k=10, L0=16, Lmax=128, eps=0.1, fused=True, warm=True)
+    assert_parity(got, ref_w, f"edge values {dtype} warm")
+    ref = oracle.boa(orc, q, r, 10, [200])
+    got = gpu_search(gpu, q, r, k=10, fixed_L=200)
+    assert_parity(got, ref, f"edge values {dtype} fixed 200")
+    gpu.close()
+
+
 @pytest.mark.parametrize("eps", [0.0, 1.0])
 def test_split_all_or_no_survivors(tiny, eps):
     """eps = 0 sends every query with more than k valid entries on to the

@@ -100,6 +100,24 @@ def test_phi_float_column_compares_as_float():
     assert oracle.phi(a, inf, t) == 0
 
 
+def test_phi_float_special_values_follow_ieee():
+    """Zeros of both signs compare equal, NaN satisfies no bound (nor does any
+    value a NaN bound), infinities and denormals order as numbers: every
+    (value, lo, hi) triple over these cells against numpy's float32 compares."""
+    cells = np.concatenate([
+        gen.f32_bits([0.0, -0.0, np.inf, -np.inf, 1e-45, -1e-45, 3.4028235e38, -3.4028235e38, 1.0, -2.5]),
+        np.array([0x7FC00000, 0xFFC00000, 0x7F800001], dtype=np.uint32).view(np.int32)])
+    f = cells.view(np.float32)
+    t = np.array([gen.ATTR_F32], dtype=np.int32)
+    for i in range(cells.size):
+        for j in range(cells.size):
+            for k in range(cells.size):
+                want = 0 if (f[j] <= f[i]) and (f[i] <= f[k]) else 1
+                assert oracle.phi(cells[i:i + 1], [[cells[j], cells[k]]], t) == want, (f[i], f[j], f[k])
+    z = gen.f32_bits([0.0, -0.0])
+    assert oracle.phi(z[1:], [[z[0], z[0]]], t) == 0 and oracle.phi(z[:1], [[z[1], z[1]]], t) == 0
+
+
 # ---------------------------------------------------------------------------
 # confidence test (Eq. 3), golden cases
 
