@@ -381,7 +381,7 @@ struct U8Scorer {
             if (PER * u >= R) break;   // uniform
             const int32_t acc = dist(rg.x[u], p, nch);
             const int cj = PER * u + g;
-            if (p == G - 1 && cj < R) cd[cj] = (float)acc;
+            if (p == G - 1) cd[cj] = (float)acc;   // (cj < 32: slots past R are not read)
         }
     }
 
@@ -734,7 +734,8 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     uint32_t *htab = reinterpret_cast<uint32_t *>(rrk + (Scorer::kPQ ? Lb : 0));   // H/2 words (H 16-bit slots)
 
     const IndexView ix = a.ix;
-    const int R = ix.R, d = ix.d, m = ix.m;
+    int R = ix.R;   // (made opaque once per expansion, see there)
+    const int d = ix.d, m = ix.m;
     // row gathers ahead of the visited test (scorers that have them, rows they cover)
     const bool spec = Scorer::kSpec && R <= Scorer::kSpecMaxR;
 
@@ -916,6 +917,19 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         uint64_t spec_key = KEY_NONE;
 
         for (;;) {
+            // Row-gather scorers re-read the row length as an opaque (uniform)
+            // value at every expansion, so that tests on it (lane < R, the
+            // number of gather rounds) are recomputed where they are used
+            // instead of being hoisted out of the loop as lane masks, which
+            // would not fit the scalar registers and would be reloaded from
+            // spill lanes at every use. (The other scorers spill more with it.
+            // The same for the lane number moves waits for the prefetched row
+            // earlier.)
+            if constexpr (Scorer::kSpec) {
+                int r = R;
+                asm volatile("" : "+v"(r));
+                R = __builtin_amdgcn_readfirstlane(r);
+            }
             uint32_t scan_from = (uint32_t)(expanded_j + 1);
             // ---- score the c new candidates listed in cid[0, c)
             PROF_T(t_score0);
