@@ -389,10 +389,10 @@ struct U8Scorer {
     // chunk p in x); the group's top lane returns it
     __device__ __forceinline__ int32_t dist(uint4 x, int p, int nch) const
     {
-        if (nch < G) {         // (uniform) lanes past the row add zero
-            if (p >= nch) x = q;
-        }
         int32_t acc = (int32_t)(dot16(x, x) + qq - 2u * dot16(x, q));
+        if (nch < G) {         // (uniform) lanes past the row add zero
+            if (p >= nch) acc = 0;
+        }
         // exact integer sum over the group; the group's top lane holds it
 #pragma unroll
         for (int s = G >> 1; s >= 16; s >>= 1) acc += __shfl_xor(acc, s);
