@@ -252,6 +252,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle timing")
     ap.add_argument("--lds-slots", type=int, default=0, help="force the LDS visited-table size")
+    ap.add_argument("--escalation-waves", type=int, default=0, choices=(0, 1),
+                    help="split mode's escalation launch: 0 two waves per query where it applies, 1 one")
     ap.add_argument("--modes", default="phased,fused,split,boa_plus,warm",
                     help="adaptive modes to time (warm: warm-start escalation, fused); the fastest of the "
                          "escalation kind chosen on the held-out batch is the headline")
@@ -352,7 +354,8 @@ def main():
     r = torch.from_numpy(data.ranges).to(dev)
     q_ho = torch.from_numpy(ho_q).to(dev)
     r_ho = torch.from_numpy(ho_r).to(dev)
-    base_kw = dict(k=wl.k, L0=wl.L0, Lmax=wl.Lmax, lds_hash_slots=args.lds_slots, pq=args.pq)
+    base_kw = dict(k=wl.k, L0=wl.L0, Lmax=wl.Lmax, lds_hash_slots=args.lds_slots, pq=args.pq,
+                   escalation_waves=args.escalation_waves)
 
     def timed(search_kw, steps, warmup, qq=q, rr=r):
         """warm-up, then `steps` timed searches bracketed by device syncs;

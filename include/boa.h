@@ -168,6 +168,13 @@ typedef struct {
                                re-rank the phase's valid worklist entries by exact
                                distance (Sec. III-B step 8); the result and Eq. 3 read
                                the re-ranked entries. k <= 128. 0: exact distances. */
+    int32_t escalation_waves; /* split mode (fused = 2), when the escalation launch keeps
+                               its visited set as an LDS bitmap over all ids and the
+                               distances are exact: 0 (default) two waves per query, one
+                               merging the worklist while the other runs the visited test,
+                               gathers and scoring of the node it expects next (the
+                               selected node when the guess misses; identical results);
+                               1: one wave per query. Ignored elsewhere. */
 } boa_params;
 
 void boa_default_params(boa_params *p);

@@ -39,7 +39,7 @@ class Params(C.Structure):
                 ("eps", C.c_double), ("tau", C.c_double), ("fixed_L", C.c_int32),
                 ("boa_plus", C.c_int32), ("sub_batches", C.c_int32), ("lds_hash_slots", C.c_int32),
                 ("schedule", C.POINTER(C.c_int32)), ("n_schedule", C.c_int32), ("fused", C.c_int32),
-                ("warm_start", C.c_int32), ("pq", C.c_int32)]
+                ("warm_start", C.c_int32), ("pq", C.c_int32), ("escalation_waves", C.c_int32)]
 
 
 class BuildParams(C.Structure):
@@ -195,7 +195,7 @@ class Index:
                sub_batches: int = 10, lds_hash_slots: int = 0, schedule=None, fused: bool = False,
                split: bool = False, counters: bool = False,
                stream=None, out=None, no_alloc: bool = False, warm: bool = False,
-               pq: bool = False) -> SearchResult:
+               pq: bool = False, escalation_waves: int = 0) -> SearchResult:
         """Adaptive filtered top-k of a batch of device-resident queries.
 
         queries: torch tensor (nq, d) on the GPU, float32 or uint8 like the index.
@@ -206,6 +206,8 @@ class Index:
                  the previous phase's list and visited set.
         pq:      traverse with product-quantised distances (set_pq first) and
                  re-rank each phase's valid entries exactly.
+        escalation_waves: split mode: 0 two waves per query in the escalation
+                 launch where it applies, 1 one wave per query.
         no_alloc: call boa_search_noalloc (the library allocates no device
                  memory for the call; pass preallocated `out` tensors to
                  allocate nothing on the torch side either).
@@ -238,6 +240,7 @@ class Index:
         p.fused = 2 if split else int(fused)
         p.warm_start = int(warm)
         p.pq = int(pq)
+        p.escalation_waves = int(escalation_waves)
         sched_arr = None
         if schedule is not None:
             sched_arr = (C.c_int32 * len(schedule))(*schedule)

@@ -552,6 +552,26 @@ int stage_profile_end(unsigned long long *prof, size_t pn, int L, int waves, hip
     (void)hipFree(prof);
     return BOA_OK;
 }
+
+// the same for the two-wave escalation launch (one row per block)
+int stage_profile_pair_end(unsigned long long *prof, size_t pn, int L, int blocks, hipStream_t st)
+{
+    std::vector<unsigned long long> h(pn);
+    HIP_TRY(hipMemcpyAsync(h.data(), prof, pn * 8, hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    double tot[BOA_PROF_SLOTS] = {0};
+    for (size_t i = 0; i < pn; ++i) tot[i % BOA_PROF_SLOTS] += (double)h[i];
+    const double ne = tot[10] > 0 ? tot[10] : 1;
+    std::fprintf(stderr,
+                 "[stage-profile] two-wave escalation L=%d blocks=%d expansions=%.0f cycles/expansion: "
+                 "iteration %.0f | worklist wave: merge and select %.0f, wait %.0f | gather wave: guessed "
+                 "expansion %.0f, wait %.0f, hand-over %.0f | guesses: hit %.3f miss %.3f none %.3f, of a new "
+                 "key %.3f; no entry after the selected one %.3f\n",
+                 L, blocks, tot[10], tot[5] / ne, tot[0] / ne, tot[3] / ne, tot[1] / ne, tot[4] / ne, tot[2] / ne,
+                 tot[8] / ne, tot[9] / ne, tot[14] / ne, tot[13] / ne, tot[12] / ne);
+    (void)hipFree(prof);
+    return BOA_OK;
+}
 #endif
 
 // A phase's launch: the automatic table of plan_phase, then doubled (up to
@@ -639,6 +659,7 @@ struct Request {
     int32_t sched[BOA_MAX_PHASES];
     int32_t n_phases;
     bool plus, split, fused, warm;
+    bool pair;                // split escalation with two waves per query where it applies
     int32_t pq_m;             // > 0: product-quantised traversal with that many subspaces
     int32_t sub;              // BOA+ sub-batches (1 otherwise)
     int32_t n_counters;
@@ -682,6 +703,9 @@ int validate(const boa_index *ix, const void *queries, const int32_t *ranges, in
     if (p->pq && ix->pq_m == 0) return fail(BOA_EINVAL, "pq = 1 needs product-quantisation codes (boa_set_pq)");
     if (p->pq && p->k > 128) return fail(BOA_EUNSUPPORTED, "a product-quantised search returns at most k = 128");
     rq.pq_m = p->pq ? ix->pq_m : 0;
+    if (p->escalation_waves != 0 && p->escalation_waves != 1)
+        return fail(BOA_EINVAL, "escalation_waves must be 0 or 1");
+    rq.pair = p->escalation_waves == 0 && rq.pq_m == 0;
     rq.sub = rq.plus ? std::min<int64_t>(p->sub_batches, std::max<int64_t>(nq, 1)) : 1;
     rq.n_counters = rq.n_phases * (rq.sub + 1) + 8;
     rq.tau_count = (uint32_t)std::floor(p->tau * (double)nq);
@@ -899,7 +923,42 @@ int run_search(boa_index *ix, const void *queries, const int32_t *ranges, int64_
                 if (int rc2 = stage_profile_begin(&prof, pn, st)) return rc2;
                 e.prof = prof;
 #endif
-                if (int rc = launch(e, pe.blocks, st, true, 1)) return rc;
+                // two waves per query where the bitmap plan applies and every
+                // survivor's block is still resident at once
+                bool pair = rq.pair && pe.vis_bitmap;
+                if (pair) {
+                    const size_t lds = pair_lds_bytes(Lw, e.vis_words,
+                                                      scorer_lds_bytes(ix->vec_dtype, ix->view.d, true, 0));
+                    const int occ = lds <= ix->lds_per_block_hw ? pair_occupancy(ix->vec_dtype, ix->view.d, lds) : 0;
+                    const int64_t cap = (int64_t)occ * ix->num_cu;
+                    pair = cap >= (int64_t)S;
+                    if (pair) {
+                        pe.blocks = (int32_t)S;
+                        pe.wpb = 2;
+                        e.lds_per_wave = (int32_t)lds;
+                        e.waves_per_block = 2;
+                    }
+                }
+                if (pair) {
+#ifdef BOA_STAGE_PROFILE
+                    unsigned long long *pprof = nullptr;
+                    const size_t ppn = (size_t)pe.blocks * BOA_PROF_SLOTS;
+                    if (int rc2 = stage_profile_begin(&pprof, ppn, st)) return rc2;
+                    e.prof = pprof;
+#endif
+                    if (ws.timing) HIP_TRY(hipEventRecord(ix->ev_start[ev], st));
+                    HIP_TRY(launch_pair(e, ix->vec_dtype, pe.blocks, st));
+                    if (ws.timing) {
+                        HIP_TRY(hipEventRecord(ix->ev_end[ev], st));
+                        ix->launch_phase.push_back({1, ev});
+                        ++ev;
+                    }
+#ifdef BOA_STAGE_PROFILE
+                    if (int rc2 = stage_profile_pair_end(pprof, ppn, Lw, (int)S, st)) return rc2;
+#endif
+                } else if (int rc = launch(e, pe.blocks, st, true, 1)) {
+                    return rc;
+                }
 #ifdef BOA_STAGE_PROFILE
                 std::fprintf(stderr, "[stage-profile] split escalation: %u survivors, table %d slots, %d waves\n",
                              S, pe.h_slots, pe.blocks * pe.wpb);

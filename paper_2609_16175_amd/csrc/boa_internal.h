@@ -152,6 +152,12 @@ int phase_occupancy(int vec_dtype, int d, int wpb, size_t lds, bool wide = false
 // per-wave LDS bytes the distance scorer keeps (its copy of the query, or
 // the product-quantisation distance table)
 int scorer_lds_bytes(int vec_dtype, int d, bool wide = false, int pq_m = 0);
+// The escalation launch of a split search with two waves per query (LDS
+// bitmap visited set, exact distances): its LDS per block, resident blocks
+// per CU, and the launch (lds_per_wave carries the block's LDS bytes).
+size_t pair_lds_bytes(int32_t L, uint32_t vis_words, int scorer_lds);
+int pair_occupancy(int vec_dtype, int d, size_t lds);
+hipError_t launch_pair(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st);
 hipError_t launch_compact(const CompactArgs &a, hipStream_t st);
 hipError_t launch_append(const AppendArgs &a, hipStream_t st);
 hipError_t launch_init(const InitArgs &a, hipStream_t st);

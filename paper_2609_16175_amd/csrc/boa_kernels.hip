@@ -1237,6 +1237,423 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
 #endif
 }
 
+// ---------------------------------------------------------------------------
+// The escalation launch of a split search with two waves per query (a
+// 128-thread block), when its visited set is the LDS bitmap over all ids.
+// One wave owns the worklist: it merges each expansion's keys and selects
+// the next node. The other owns the bitmap: it tests a row's neighbours,
+// gathers and scores the new ones. The expansions stay one node at a time
+// in the order of Alg. 2; what overlaps is the guess of the next node. After
+// handing over an expansion's keys, the gather wave takes as the next node
+// the smaller of its best new key and the entry that followed the expanded
+// one (the selection after the merge is exactly that whenever the entry is
+// known), and runs that node's visited test, gathers and scoring while the
+// worklist wave merges. If the selection differs, the guessed node's bits are
+// cleared again (the gather wave is the only writer of the bitmap, so the set
+// returns to its state before the guess) and the selected node is expanded.
+// The visited set sees the same inserts in the same order, so results and
+// counts are those of the one-wave launch.
+//
+// Control flow that both waves share (the query loop, the phase loop, the
+// end of a phase's search) is decided from values they read from LDS after
+// the same block barrier, so both run the same sequence of barriers.
+struct PairCtrl {
+    uint64_t kn;       // the entry after the selected one (KEY_NONE: not known)
+    uint32_t t;        // query slot taken by the block
+    uint32_t sel;      // the selected node's id, or PAIR_DONE
+    uint32_t S;        // scored nodes of the phase (gather wave)
+    uint32_t last;     // the query's result has been written
+    uint32_t pad[2];
+};
+static constexpr uint32_t PAIR_DONE = 0xFFFFFFFFu;
+
+template <class Scorer>
+__global__ void __launch_bounds__(128) pair_kernel(PhaseArgs a)
+{
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int lane = lane_id();
+    const bool merger = threadIdx.x < 64;   // wave 0: worklist; wave 1: bitmap and scoring
+    const int Lb = beam_slots(a.L_alloc);
+    const int pw = ((a.L_alloc >> 6) + 3) & ~1;
+    uint64_t *beam = reinterpret_cast<uint64_t *>(smem);        // Lb
+    uint64_t *nkey = beam + Lb;                                   // 64
+    uint64_t *posbm = nkey + 64;                                  // pw
+    uint64_t *kbuf = posbm + pw;                                  // 64: an expansion's keys
+    uint32_t *krow = reinterpret_cast<uint32_t *>(kbuf + 64);   // 64: the row of ctl->kn
+    PairCtrl *ctl = reinterpret_cast<PairCtrl *>(krow + 64);
+    uint32_t *cid = reinterpret_cast<uint32_t *>(ctl + 1);      // 64
+    float *cd = reinterpret_cast<float *>(cid + 64);             // 64
+    unsigned char *qlds = reinterpret_cast<unsigned char *>(cd + 64);
+    uint32_t *bits = reinterpret_cast<uint32_t *>(qlds + Scorer::kLdsBytes);   // vis_words
+
+    const IndexView ix = a.ix;
+    const int R = ix.R, d = ix.d, m = ix.m;
+    const uint32_t n_in = bcast0(*a.n_active);
+    if (n_in <= a.tau_count) return;   // (the same for both waves)
+    const uint32_t nA = a.t_end < n_in ? a.t_end : n_in;
+
+    Scorer sc;
+    sc.bind_lds(qlds);
+    // the gather wave's attribute test (as in phase_kernel)
+    int32_t flo[BOA_MAX_M];
+    uint32_t fspan[BOA_MAX_M];
+    uint32_t phi0 = 0;
+    auto load_attrs = [&](uint32_t id, int4 &w0, int4 &w1) {
+        const int32_t *ar = ix.attrs + (size_t)id * ix.m_pad;
+        if (ix.m_pad >= 4) {
+            w0 = reinterpret_cast<const int4 *>(ar)[0];
+            if (ix.m_pad == 8) w1 = reinterpret_cast<const int4 *>(ar)[1];
+        } else if (ix.m_pad == 2) {
+            const int2 t2 = reinterpret_cast<const int2 *>(ar)[0];
+            w0.x = t2.x;
+            w0.y = t2.y;
+        } else {
+            w0.x = ar[0];
+        }
+    };
+    auto count_phi = [&](const int4 &w0, const int4 &w1) -> uint32_t {
+        const int32_t av[BOA_MAX_M] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+        auto cells = [&](auto nc_tag) -> uint32_t {
+            constexpr int NC = decltype(nc_tag)::value;
+            uint32_t phi = phi0;
+#pragma unroll
+            for (int j = 0; j < NC; ++j) phi += (uint32_t)(av[j] - flo[j]) > fspan[j] ? 1u : 0u;
+            return phi;
+        };
+        switch (ix.m_pad) {
+        case 1: return cells(std::integral_constant<int, 1>{});
+        case 2: return cells(std::integral_constant<int, 2>{});
+        case 4: return cells(std::integral_constant<int, 4>{});
+        default: return cells(std::integral_constant<int, 8>{});
+        }
+    };
+    // keys of the candidates cid[0, c): one per lane, KEY_NONE past c
+    auto score_cands = [&](uint32_t c) -> uint64_t {
+        if (c == 0) return KEY_NONE;
+        wave_sync();
+        const uint32_t my_id = cid[lane];
+        typename Scorer::Ids ids0;
+        sc.read_ids(cid, (int)c, 0, lane, ids0);
+        int4 w0 = make_int4(0, 0, 0, 0), w1 = make_int4(0, 0, 0, 0);
+        if (lane < (int)c) load_attrs(my_id, w0, w1);
+        sc.score(ix.vectors, d, cid, (int)c, cd, lane, ids0);
+        const uint32_t phi = count_phi(w0, w1);
+        wave_sync();
+        return lane < (int)c ? make_key(phi, cd[lane], cid[lane]) : KEY_NONE;
+    };
+    // test-and-insert of a row (one neighbour per lane); the new ones go to
+    // cid in lane order
+    auto visit_row = [&](uint32_t v, uint64_t &nm) -> uint32_t {
+        bool is_new = false;
+        if (v != BOA_PAD) {
+            const uint32_t bit = 1u << (v & 31u);
+            is_new = (atomicOr(&bits[v >> 5], bit) & bit) == 0u;
+        }
+        nm = __ballot(is_new);
+        if (is_new) cid[lanes_below(nm)] = v;
+        return (uint32_t)__popcll(nm);
+    };
+    auto undo_row = [&](uint32_t v, uint64_t nm) {
+        if ((nm >> lane) & 1ull) atomicAnd(&bits[v >> 5], ~(1u << (v & 31u)));
+        wave_sync();
+    };
+    auto row_of = [&](uint32_t u) -> uint32_t { return lane < R ? ix.adj[(size_t)u * R + lane] : BOA_PAD; };
+#ifdef BOA_STAGE_PROFILE
+    // worklist wave: 0 merge and select, 3 wait for the guess, 5 whole
+    // iteration, 10 expansions; gather wave: 1 guessed expansion, 4 wait for
+    // the selection, 2 hand-over (and the expansion after a miss), 8 hits,
+    // 9 misses, 14 no guess, 13 guesses of a new key; 12 (worklist wave) no
+    // entry known after the selected one
+    uint64_t prof_acc[BOA_PROF_SLOTS] = {};
+#endif
+
+    for (;;) {
+        if (merger && lane == 0) ctl->t = atomicAdd(a.queue, 1u);
+        __syncthreads();
+        const uint32_t t = bcast0(ctl->t) + a.t_begin;
+        if (t >= nA) break;   // (both waves)
+        const uint32_t qi = bcast0(a.active[t]);
+        if (!merger) {
+            sc.load_query(a.queries, qi, d, lane);
+            phi0 = 0;
+#pragma unroll
+            for (int j = 0; j < BOA_MAX_M; ++j) {
+                int32_t l = 0;
+                uint32_t s = 0xFFFFFFFFu;
+                if (j < m) {
+                    int32_t lo = a.ranges[((size_t)qi * m + j) * 2 + 0];
+                    int32_t hi = a.ranges[((size_t)qi * m + j) * 2 + 1];
+                    bool none = false;
+                    if ((ix.f32_mask >> j) & 1u) {
+                        none = ((uint32_t)lo & 0x7FFFFFFFu) > 0x7F800000u ||
+                               ((uint32_t)hi & 0x7FFFFFFFu) > 0x7F800000u;
+                        lo = f32_ord((uint32_t)lo);
+                        hi = f32_ord((uint32_t)hi);
+                    }
+                    if (none || lo > hi) {
+                        phi0 += 1;
+                    } else {
+                        l = lo;
+                        s = (uint32_t)hi - (uint32_t)lo;
+                    }
+                }
+                asm volatile("" : "+v"(l), "+v"(s));
+                flo[j] = l;
+                fspan[j] = s;
+            }
+        }
+        // every phase restarts from the entry point (Alg. 1 calls Alg. 2 afresh)
+        for (int p = a.p_begin; p < a.p_end; ++p) {
+            const int L = a.sched[p];
+            // worklist wave
+            uint32_t len = 0, E = 0;
+            int expanded_j = -1;
+            // gather wave: the keys of the last expansion handed over, the
+            // entry known to follow the last selected node, its row in flight,
+            // and the guessed expansion (row, new-neighbour mask, keys)
+            uint32_t S = 0;
+            uint64_t ckey = KEY_NONE, kn_prev = KEY_NONE;
+            uint32_t kn_row = BOA_PAD;   // row of kn_prev (read from krow)
+            bool guess = false;
+            uint32_t g_id = BOA_PAD, g_v = BOA_PAD, g_c = 0;
+            uint64_t g_nm = 0, g_key = KEY_NONE;
+            if (merger) {
+                for (int i = lane; i < Lb; i += 64) beam[i] = KEY_NONE;
+            } else {
+                const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+                uint4 *b4 = reinterpret_cast<uint4 *>(bits);
+                for (uint32_t i = lane; i < (a.vis_words >> 2); i += 64) b4[i] = z;
+                wave_sync();
+                if (lane == 0) {
+                    bits[ix.entry >> 5] |= 1u << (ix.entry & 31u);
+                    cid[0] = ix.entry;
+                }
+                ckey = score_cands(1u);   // the entry point, scored before the first expansion
+                S = 1;
+                kbuf[lane] = ckey;
+            }
+            for (;;) {
+                __syncthreads();   // kbuf holds the last expansion's keys
+                PROF_T(t_b1);
+                if (merger) {
+                    // ---- drop, sort and merge the keys (as in phase_kernel)
+                    uint64_t key = kbuf[lane];
+                    uint32_t scan_from = (uint32_t)(expanded_j + 1);
+                    if (len == (uint32_t)L && key >= beam[L - 1]) key = KEY_NONE;   // cannot enter
+                    const uint64_t keep = __ballot(key != KEY_NONE);
+                    const uint32_t kept = __popcll(keep);
+                    if (kept > 0) {
+                        nkey[key != KEY_NONE ? lanes_below(keep) : kept + lanes_below(~keep)] = key;
+                        wave_sync();
+                        uint32_t rank = 0;
+                        {
+                            const ulonglong2 *nk2 = reinterpret_cast<const ulonglong2 *>(nkey);
+                            for (uint32_t i = 0; i < kept; i += 8) {
+                                const ulonglong2 a0 = nk2[(i >> 1) + 0], a1 = nk2[(i >> 1) + 1];
+                                const ulonglong2 a2 = nk2[(i >> 1) + 2], a3 = nk2[(i >> 1) + 3];
+                                rank += (a0.x < key ? 1u : 0u) + (a0.y < key ? 1u : 0u);
+                                rank += (a1.x < key ? 1u : 0u) + (a1.y < key ? 1u : 0u);
+                                rank += (a2.x < key ? 1u : 0u) + (a2.y < key ? 1u : 0u);
+                                rank += (a3.x < key ? 1u : 0u) + (a3.y < key ? 1u : 0u);
+                            }
+                        }
+                        wave_sync();
+                        if (key != KEY_NONE) nkey[rank] = key;
+                        wave_sync();
+                        key = lane < (int)kept ? nkey[lane] : KEY_NONE;
+                        uint32_t f = 0xFFFFFFFFu, pos = 0;
+                        if (lane < (int)kept) {
+                            pos = lower_bound64_p2(beam, (uint32_t)beam_slots((int32_t)len), key);
+                            f = pos + lane;
+                        }
+                        const uint32_t p0 = bcast0(pos);
+                        const uint32_t newlen = min((uint32_t)L, len + kept);
+                        const uint32_t w_lo = bcast0(p0 >> 6), w_hi = bcast0((newlen - 1u) >> 6);
+                        for (uint32_t w = w_lo + lane; w <= w_hi; w += 64) posbm[w] = 0ull;
+                        wave_sync();
+                        const bool placed = f < (uint32_t)L;
+                        if (placed) atomicOr(reinterpret_cast<unsigned long long *>(&posbm[f >> 6]),
+                                             1ull << (f & 63u));
+                        const uint32_t n_placed = __popcll(__ballot(placed));
+                        wave_sync();
+                        uint64_t word = posbm[w_hi];
+                        uint32_t below = n_placed - (uint32_t)__popcll(word);
+                        for (int w = (int)w_hi; w >= (int)w_lo; --w) {
+                            const uint32_t o = ((uint32_t)w << 6) + lane;
+                            const bool act = o >= p0 && o < newlen;
+                            const bool isnew = (word >> lane) & 1ull;
+                            const uint32_t cnt = below + (uint32_t)__popcll(word & ((1ull << lane) - 1ull));
+                            uint64_t val = 0;
+                            if (act) val = isnew ? nkey[cnt] : beam[o - cnt];
+                            wave_sync();
+                            if (act) beam[o] = val;
+                            if (w > (int)w_lo) {
+                                word = posbm[w - 1];
+                                below -= (uint32_t)__popcll(word);
+                            }
+                            wave_sync();
+                        }
+                        len = newlen;
+                        if (p0 < scan_from) scan_from = p0;
+                    }
+                    // ---- select the first unexpanded entry among the first L,
+                    // and the one after it when the same scan sees it
+                    const uint32_t lim = min(len, (uint32_t)L);
+                    int j = -1, j2 = -1;
+                    uint64_t ku = 0, kn = KEY_NONE;
+                    for (uint32_t b0 = scan_from; b0 < lim; b0 += 64) {
+                        const uint32_t i = b0 + lane;
+                        const uint64_t bk = i < lim ? beam[i] : 1ull;
+                        const uint64_t mk = __ballot(!(bk & 1ull));
+                        if (mk) {
+                            const int l1 = __ffsll((unsigned long long)mk) - 1;
+                            j = (int)b0 + l1;
+                            ku = readlane64(bk, l1);
+                            const uint64_t rest = mk & (mk - 1ull);
+                            if (rest) {
+                                const int l2 = __ffsll((unsigned long long)rest) - 1;
+                                j2 = (int)b0 + l2;
+                                kn = readlane64(bk, l2);
+                            }
+                            break;
+                        }
+                    }
+                    wave_sync();
+                    if (j >= 0) {
+                        expanded_j = j;
+                        E += 1;
+                        if (lane == 0) beam[j] = ku | 1ull;
+                    }
+                    if (lane == 0) {
+                        ctl->sel = j >= 0 ? key_id(ku) : PAIR_DONE;
+                        ctl->kn = j2 >= 0 ? kn : KEY_NONE;
+                    }
+                    // the row of the entry after the selected node, for the
+                    // gather wave's next guess (this wave waits at the barrier
+                    // for the guessed expansion anyway)
+                    if (j2 >= 0) krow[lane] = lane < R ? ix.adj[(size_t)key_id(kn) * R + lane] : BOA_PAD;
+                    PROF_T(t_m1);
+                    PROF_ADD(0, t_m1 - t_b1);
+                    PROF_ADD(10, j >= 0 ? 1 : 0);
+                    PROF_ADD(12, j >= 0 && j2 < 0 ? 1 : 0);
+                } else {
+                    // ---- the guessed next node: visited test, gathers, keys
+                    const uint64_t mk = wave_min64(ckey);
+                    const uint64_t gk = mk < kn_prev ? mk : kn_prev;
+                    guess = gk != KEY_NONE;
+                    if (guess) {
+                        g_id = key_id(gk);
+                        // the entry after the last selected node: its row came
+                        // from the worklist wave; a new key: its row is loaded
+                        // now. (A row of the best new key requested ahead was
+                        // measured slower: the compiler waits for it before the
+                        // gathers of the next expansion, whichever row is used.)
+                        if (bcast0(gk == kn_prev ? 1u : 0u)) {   // (uniform: a scalar branch)
+                            g_v = kn_row;
+                        } else {
+                            g_v = row_of(g_id);
+                            PROF_ADD(13, 1);
+                        }
+                        g_c = visit_row(g_v, g_nm);
+                        g_key = score_cands(g_c);
+                    }
+                    PROF_T(t_g1);
+                    PROF_ADD(1, t_g1 - t_b1);
+                }
+                PROF_T(t_pre2);
+                __syncthreads();   // the selection is published
+                PROF_T(t_b2);
+                PROF_ADD(merger ? 3 : 4, t_b2 - t_pre2);
+                const uint32_t sel = bcast0(ctl->sel);
+                if (sel == PAIR_DONE) {   // converged (both waves)
+                    if (!merger && guess) undo_row(g_v, g_nm);
+                    break;
+                }
+                if (!merger) {
+                    const uint64_t kn_new = ctl->kn;
+                    uint32_t c;
+                    PROF_ADD(guess ? (g_id == sel ? 8 : 9) : 14, 1);
+                    if (guess && g_id == sel) {
+                        ckey = g_key;
+                        c = g_c;
+                    } else {
+                        if (guess) undo_row(g_v, g_nm);
+                        uint64_t nm;
+                        const uint32_t v = sel == key_id(kn_prev) && kn_prev != KEY_NONE ? kn_row : row_of(sel);
+                        c = visit_row(v, nm);
+                        ckey = score_cands(c);
+                    }
+                    S += c;
+                    kbuf[lane] = ckey;
+                    // the entry after the selected node and its row, which the
+                    // worklist wave loaded
+                    kn_prev = kn_new;
+                    kn_row = krow[lane];
+                    PROF_T(t_g2);
+                    PROF_ADD(2, t_g2 - t_b2);
+                }
+                if (merger) {
+                    PROF_T(t_m2);
+                    PROF_ADD(5, t_m2 - t_b1);
+                }
+            }
+            // ---- epilogue (worklist wave): Eq. 3 over the first L entries
+            if (!merger && lane == 0) ctl->S = S;
+            __syncthreads();
+            if (merger) {
+                const uint32_t n_valid = lower_bound64(beam, min(len, (uint32_t)L), KEY_PHI1);
+                const int k = a.k;
+                uint32_t conf = 0;
+                if (n_valid > (uint32_t)k) {
+                    const double dk = sqrt((double)key_dist(beam[k - 1]));
+                    const double dmax = sqrt((double)key_dist(beam[n_valid - 1]));
+                    const double gamma = dmax == 0.0 ? 0.0 : (dmax - dk) / dmax;
+                    conf = gamma <= a.eps ? 1u : 0u;
+                }
+                const bool last = conf != 0u || p + 1 == a.p_end;
+                const uint32_t Sp = bcast0(ctl->S);
+                if (lane == 0) {
+                    const size_t ps = (size_t)p * a.nq + qi;
+                    if (a.qstat) {
+                        a.qstat[ps] = (uint8_t)(1u + conf);
+                        a.qE[ps] = E;
+                        a.qS[ps] = Sp;
+                    }
+                    if (a.user_E) a.user_E[qi] += E;
+                    if (a.user_S) a.user_S[qi] += Sp;
+                    if (a.write_conf) a.conf[t] = (uint8_t)conf;
+                    if (last) a.final_L[qi] = L;
+                    ctl->last = last ? 1u : 0u;
+                }
+                if (last) {
+                    for (int q = lane; q < k; q += 64) {
+                        uint32_t id = BOA_PAD;
+                        float dd = __int_as_float(0x7f800000);
+                        if ((uint32_t)q < n_valid) {
+                            id = key_id(beam[q]);
+                            dd = key_dist(beam[q]);
+                        }
+                        a.ids[(size_t)qi * k + q] = id;
+                        a.dists[(size_t)qi * k + q] = dd;
+                    }
+                }
+            }
+            __syncthreads();
+            if (bcast0(ctl->last)) break;   // (both waves)
+        }   // phases
+    }       // queries
+#ifdef BOA_STAGE_PROFILE
+    if (lane == 0 && a.prof) {
+        static constexpr int mine_m[] = {0, 3, 5, 10, 12};
+        static constexpr int mine_g[] = {1, 2, 4, 8, 9, 13, 14};
+        if (merger)
+            for (int i : mine_m) a.prof[(size_t)blockIdx.x * BOA_PROF_SLOTS + i] += prof_acc[i];
+        else
+            for (int i : mine_g) a.prof[(size_t)blockIdx.x * BOA_PROF_SLOTS + i] += prof_acc[i];
+    }
+#endif
+}
+
 // Stable compaction of the active list (Alg. 1: survivors escalate). One
 // block: flags -> ballot prefix within waves -> wave totals in LDS.
 __global__ void __launch_bounds__(1024) compact_kernel(CompactArgs a)
@@ -1380,6 +1797,43 @@ static int occupancy_t(int wpb, size_t lds)
         else if (WIDE) BOA_DISPATCH_W(VEC, DIM, 2, CALL);                    \
         else BOA_DISPATCH_W(VEC, DIM, 1, CALL);                              \
     } while (0)
+
+template <class Scorer>
+static hipError_t launch_pair_t(const PhaseArgs &a, int blocks, hipStream_t st)
+{
+    hipLaunchKernelGGL(pair_kernel<Scorer>, dim3(blocks), dim3(128), (size_t)a.lds_per_wave, st, a);
+    return hipGetLastError();
+}
+
+template <class Scorer>
+static int pair_occupancy_t(size_t lds)
+{
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, pair_kernel<Scorer>, 128, lds) != hipSuccess) return 0;
+    return nb;
+}
+
+// the two-wave escalation launch (wide scorers; lds_per_wave is the block's LDS)
+hipError_t launch_pair(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st)
+{
+    hipError_t e = hipSuccess;
+    BOA_DISPATCH_W(vec_dtype, a.ix.d, 2, e = launch_pair_t<S_>(a, blocks, st));
+    return e;
+}
+
+int pair_occupancy(int vec_dtype, int d, size_t lds)
+{
+    int r = 0;
+    BOA_DISPATCH_W(vec_dtype, d, 2, r = pair_occupancy_t<S_>(lds));
+    return r;
+}
+
+size_t pair_lds_bytes(int32_t L, uint32_t vis_words, int scorer_lds)
+{
+    const int32_t Lb = beam_slots(L), pw = ((L >> 6) + 3) & ~1;
+    return (size_t)8 * Lb + 8 * 64 + 8 * (size_t)pw + 8 * 64 + 4 * 64 + sizeof(PairCtrl) + 4 * 64 + 4 * 64 +
+           (size_t)scorer_lds + 4 * (size_t)vis_words;
+}
 
 hipError_t launch_phase(const PhaseArgs &a, int vec_dtype, int blocks, hipStream_t st, bool wide)
 {

@@ -34,9 +34,11 @@ def test_library_exports_every_declared_symbol():
 def test_struct_layouts_match_header():
     # sizes follow from the header's field order on x86-64
     # k, L0, Lmax, pad, alpha, eps, tau, fixed_L, boa_plus, sub_batches,
-    # lds_hash_slots, schedule, n_schedule, fused, warm_start, pq
-    assert C.sizeof(boa.Params) == 4 * 3 + 4 + 8 * 3 + 4 * 4 + 8 + 4 + 4 + 4 + 4
+    # lds_hash_slots, schedule, n_schedule, fused, warm_start, pq,
+    # escalation_waves, tail padding to the struct's 8-byte alignment
+    assert C.sizeof(boa.Params) == 4 * 3 + 4 + 8 * 3 + 4 * 4 + 8 + 4 + 4 + 4 + 4 + 4 + 4
     assert boa.Params.warm_start.offset == 72 and boa.Params.pq.offset == 76
+    assert boa.Params.escalation_waves.offset == 80
     assert C.sizeof(boa.PhaseStats) == 4 * 4 + 8 * 2 + 8 + 4 + 4
 
 
@@ -44,6 +46,7 @@ def test_default_params():
     p = boa.default_params()
     assert (p.k, p.L0, p.Lmax, p.alpha, p.eps, p.tau) == (10, 16, 512, 2.0, 0.05, 0.0)
     assert p.fixed_L == 0 and p.boa_plus == 0 and p.sub_batches == 10
+    assert p.escalation_waves == 0
 
 
 def _build(**over):

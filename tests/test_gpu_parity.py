@@ -126,10 +126,34 @@ def test_split_escalation_bitmap_and_table(tiny, eps):
     sched = oracle.schedule(wl.L0, 2.0, wl.Lmax)
     ref = oracle.boa(tiny["orc"], d.queries, d.ranges, wl.k, sched, eps=eps)
     assert ref.phases[1]["active"] > 0
-    for slots in (0, 4096):
+    for slots, waves in ((0, 0), (0, 1), (4096, 0)):
         got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, L0=wl.L0, Lmax=wl.Lmax, eps=eps,
-                         split=True, lds_hash_slots=slots)
-        assert_parity(got, ref, f"split eps={eps} slots={slots}")
+                         split=True, lds_hash_slots=slots, escalation_waves=waves)
+        assert_parity(got, ref, f"split eps={eps} slots={slots} escalation_waves={waves}")
+
+
+@pytest.mark.parametrize("eps", [0.0, 0.02, 0.05])
+def test_split_two_wave_escalation(tiny, eps):
+    """The escalation launch with two waves per query (one merging the
+    worklist, one expanding the node it expects next and taking the guess
+    back when the selection differs) against the oracle and the one-wave
+    launch. Widths 10, 20, 40, 80: no query is confident at 10 (it needs
+    more than k valid entries), some stop at 20 inside the escalation launch
+    (eps 0.02: 27 of 100), the rest run to 80. Twice with two waves."""
+    wl, d = tiny["wl"], tiny["data"]
+    sched = [10, 20, 40, 80]
+    ref = oracle.boa(tiny["orc"], d.queries, d.ranges, 10, sched, eps=eps)
+    assert ref.phases[1]["active"] == d.queries.shape[0]
+    for waves in (0, 1, 0):
+        got = gpu_search(tiny["gpu"], d.queries, d.ranges, k=10, schedule=sched, eps=eps,
+                         split=True, escalation_waves=waves)
+        assert_parity(got, ref, f"split eps={eps} escalation_waves={waves}")
+        st = tiny["gpu"].stats()
+        for p, rp in zip(st["phases"], ref.phases):
+            assert (p["active"], p["confident"], p["expansions"], p["scored"]) == \
+                (rp["active"], rp["confident"], rp["expansions"], rp["scored"])
+    with pytest.raises(_boa().BoaError):
+        gpu_search(tiny["gpu"], d.queries, d.ranges, k=wl.k, split=True, escalation_waves=2)
 
 
 @pytest.mark.parametrize("mode", list(MODES))
