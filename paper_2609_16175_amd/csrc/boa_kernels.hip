@@ -24,6 +24,10 @@
 // The epilogue writes the first k filter-valid entries, the phase width,
 // and the Eq. 3 confidence flag.
 //
+// The escalation launch of a split search can instead give each query two
+// waves (pair_kernel, below): one merges and selects while the other runs
+// the visited test, gathers and scoring of the node it expects next.
+//
 // Worklist key (unsigned 64-bit, compared as an integer):
 //   bits 63..60 phi (violations, <= 8), bits 59..28 float32 bits of the
 //   squared distance (non-negative floats order like their bit patterns),
@@ -572,6 +576,87 @@ __device__ __forceinline__ uint64_t wave_min64(uint64_t v)
 }
 
 // ---------------------------------------------------------------------------
+// Attribute filter (Eq. 2). A point's record is m_pad cells, loaded as one
+// aligned vector load (int4 halves w0, w1). The index holds float32 cells
+// as order-preserving integers (f32_ord), and RangeTest maps each query's
+// bounds the same way, so a cell satisfies its range [lo, hi] exactly when
+// (uint32)(x - lo) <= hi - lo. A range that nothing satisfies (lo > hi, or a
+// NaN bound of a float32 column, which fails every comparison) counts in
+// phi0 for every point; its cell, like a padding cell, then passes.
+
+__device__ __forceinline__ void load_attr_record(const IndexView &ix, uint32_t id, int4 &w0, int4 &w1)
+{
+    const int32_t *ar = ix.attrs + (size_t)id * ix.m_pad;
+    if (ix.m_pad >= 4) {
+        w0 = reinterpret_cast<const int4 *>(ar)[0];
+        if (ix.m_pad == 8) w1 = reinterpret_cast<const int4 *>(ar)[1];
+    } else if (ix.m_pad == 2) {
+        const int2 t2 = reinterpret_cast<const int2 *>(ar)[0];
+        w0.x = t2.x;
+        w0.y = t2.y;
+    } else {
+        w0.x = ar[0];
+    }
+}
+
+struct RangeTest {
+    int32_t flo[BOA_MAX_M];
+    uint32_t fspan[BOA_MAX_M];
+    uint32_t phi0;
+
+    // query qi's m ranges (row-major nq x m x 2 cells)
+    __device__ __forceinline__ void set(const int32_t *ranges, uint32_t qi, int m, uint32_t f32_mask)
+    {
+        phi0 = 0;
+#pragma unroll
+        for (int j = 0; j < BOA_MAX_M; ++j) {
+            int32_t l = 0;
+            uint32_t s = 0xFFFFFFFFu;   // (padding cells pass)
+            if (j < m) {
+                int32_t lo = ranges[((size_t)qi * m + j) * 2 + 0];
+                int32_t hi = ranges[((size_t)qi * m + j) * 2 + 1];
+                bool none = false;
+                if ((f32_mask >> j) & 1u) {
+                    none = ((uint32_t)lo & 0x7FFFFFFFu) > 0x7F800000u || ((uint32_t)hi & 0x7FFFFFFFu) > 0x7F800000u;
+                    lo = f32_ord((uint32_t)lo);
+                    hi = f32_ord((uint32_t)hi);
+                }
+                if (none || lo > hi) {
+                    phi0 += 1;
+                } else {
+                    l = lo;
+                    s = (uint32_t)hi - (uint32_t)lo;
+                }
+            }
+            // (held in vector registers: kept uniform they would be spilled
+            // scalars, reloaded at every use)
+            asm volatile("" : "+v"(l), "+v"(s));
+            flo[j] = l;
+            fspan[j] = s;
+        }
+    }
+
+    // phi of a record: its m_pad cells (one uniform dispatch, no per-cell tests)
+    __device__ __forceinline__ uint32_t phi(const int4 &w0, const int4 &w1, int m_pad) const
+    {
+        const int32_t av[BOA_MAX_M] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+        auto cells = [&](auto nc_tag) -> uint32_t {
+            constexpr int NC = decltype(nc_tag)::value;
+            uint32_t p = phi0;
+#pragma unroll
+            for (int j = 0; j < NC; ++j) p += (uint32_t)(av[j] - flo[j]) > fspan[j] ? 1u : 0u;
+            return p;
+        };
+        switch (m_pad) {
+        case 1: return cells(std::integral_constant<int, 1>{});
+        case 2: return cells(std::integral_constant<int, 2>{});
+        case 4: return cells(std::integral_constant<int, 4>{});
+        default: return cells(std::integral_constant<int, 8>{});
+        }
+    }
+};
+
+// ---------------------------------------------------------------------------
 // Visited set (exact). LDS part: a two-choice bucketed table of 16-bit
 // entries. A bijective mix of the id's B bits gives h; its top bits select
 // the home bucket b1, the low r = B - log2(buckets) <= 15 bits are stored.
@@ -761,46 +846,10 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
     Scorer sc;
     sc.bind_lds(qlds);
     if constexpr (Scorer::kPQ) sc.bind_pq(a.pq_codes, a.pq_m, a.pq_cb, d, a.vec_u8);
-    // one point's attribute record (m_pad cells) and its violation count
-    auto load_attrs = [&](uint32_t id, int4 &w0, int4 &w1) {
-        const int32_t *ar = ix.attrs + (size_t)id * ix.m_pad;
-        if (ix.m_pad >= 4) {
-            w0 = reinterpret_cast<const int4 *>(ar)[0];
-            if (ix.m_pad == 8) w1 = reinterpret_cast<const int4 *>(ar)[1];
-        } else if (ix.m_pad == 2) {
-            const int2 t2 = reinterpret_cast<const int2 *>(ar)[0];
-            w0.x = t2.x;
-            w0.y = t2.y;
-        } else {
-            w0.x = ar[0];
-        }
-    };
-    // Eq. 2's phi: the number of violated predicates. The index holds float32
-    // cells as order-preserving integers, and each query's bounds are mapped
-    // the same way, so a cell satisfies its range [lo, hi] exactly when
-    // (uint32)(x - lo) <= hi - lo. A range that nothing satisfies (lo > hi, or
-    // a NaN bound of a float32 column, which fails every comparison) counts
-    // in phi0 for every point; its cell, like a padding cell, then passes.
-    int32_t flo[BOA_MAX_M];
-    uint32_t fspan[BOA_MAX_M];
-    uint32_t phi0 = 0;
-    auto count_phi = [&](const int4 &w0, const int4 &w1) -> uint32_t {
-        const int32_t av[BOA_MAX_M] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-        // the record's m_pad cells (one uniform dispatch, no per-cell tests)
-        auto cells = [&](auto nc_tag) -> uint32_t {
-            constexpr int NC = decltype(nc_tag)::value;
-            uint32_t phi = phi0;
-#pragma unroll
-            for (int j = 0; j < NC; ++j) phi += (uint32_t)(av[j] - flo[j]) > fspan[j] ? 1u : 0u;
-            return phi;
-        };
-        switch (ix.m_pad) {
-        case 1: return cells(std::integral_constant<int, 1>{});
-        case 2: return cells(std::integral_constant<int, 2>{});
-        case 4: return cells(std::integral_constant<int, 4>{});
-        default: return cells(std::integral_constant<int, 8>{});
-        }
-    };
+    // one point's attribute record (m_pad cells) and its violation count (Eq. 2)
+    auto load_attrs = [&](uint32_t id, int4 &w0, int4 &w1) { load_attr_record(ix, id, w0, w1); };
+    RangeTest rt;
+    auto count_phi = [&](const int4 &w0, const int4 &w1) -> uint32_t { return rt.phi(w0, w1, ix.m_pad); };
 #ifdef BOA_STAGE_PROFILE
     uint64_t prof_acc[BOA_PROF_SLOTS] = {};
 #endif
@@ -812,33 +861,7 @@ __global__ void __launch_bounds__(256) phase_kernel(PhaseArgs a)
         const uint32_t qi = bcast0(a.active[t]);
 
         sc.load_query(a.queries, qi, d, lane);
-        phi0 = 0;
-#pragma unroll
-        for (int j = 0; j < BOA_MAX_M; ++j) {
-            int32_t l = 0;
-            uint32_t s = 0xFFFFFFFFu;   // (padding cells pass)
-            if (j < m) {
-                int32_t lo = a.ranges[((size_t)qi * m + j) * 2 + 0];
-                int32_t hi = a.ranges[((size_t)qi * m + j) * 2 + 1];
-                bool none = false;
-                if ((ix.f32_mask >> j) & 1u) {
-                    none = ((uint32_t)lo & 0x7FFFFFFFu) > 0x7F800000u || ((uint32_t)hi & 0x7FFFFFFFu) > 0x7F800000u;
-                    lo = f32_ord((uint32_t)lo);
-                    hi = f32_ord((uint32_t)hi);
-                }
-                if (none || lo > hi) {
-                    phi0 += 1;
-                } else {
-                    l = lo;
-                    s = (uint32_t)hi - (uint32_t)lo;
-                }
-            }
-            // (held in vector registers: kept uniform they would be spilled
-            // scalars, reloaded at every use)
-            asm volatile("" : "+v"(l), "+v"(s));
-            flo[j] = l;
-            fspan[j] = s;
-        }
+        rt.set(a.ranges, qi, m, ix.f32_mask);
         // the phases of this launch: each restarts the search from the entry
         // point at its own width (Alg. 1 calls Alg. 2 afresh)
         // search state; in the warm-start mode it carries over from phase to
@@ -1294,39 +1317,7 @@ __global__ void __launch_bounds__(128) pair_kernel(PhaseArgs a)
 
     Scorer sc;
     sc.bind_lds(qlds);
-    // the gather wave's attribute test (as in phase_kernel)
-    int32_t flo[BOA_MAX_M];
-    uint32_t fspan[BOA_MAX_M];
-    uint32_t phi0 = 0;
-    auto load_attrs = [&](uint32_t id, int4 &w0, int4 &w1) {
-        const int32_t *ar = ix.attrs + (size_t)id * ix.m_pad;
-        if (ix.m_pad >= 4) {
-            w0 = reinterpret_cast<const int4 *>(ar)[0];
-            if (ix.m_pad == 8) w1 = reinterpret_cast<const int4 *>(ar)[1];
-        } else if (ix.m_pad == 2) {
-            const int2 t2 = reinterpret_cast<const int2 *>(ar)[0];
-            w0.x = t2.x;
-            w0.y = t2.y;
-        } else {
-            w0.x = ar[0];
-        }
-    };
-    auto count_phi = [&](const int4 &w0, const int4 &w1) -> uint32_t {
-        const int32_t av[BOA_MAX_M] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-        auto cells = [&](auto nc_tag) -> uint32_t {
-            constexpr int NC = decltype(nc_tag)::value;
-            uint32_t phi = phi0;
-#pragma unroll
-            for (int j = 0; j < NC; ++j) phi += (uint32_t)(av[j] - flo[j]) > fspan[j] ? 1u : 0u;
-            return phi;
-        };
-        switch (ix.m_pad) {
-        case 1: return cells(std::integral_constant<int, 1>{});
-        case 2: return cells(std::integral_constant<int, 2>{});
-        case 4: return cells(std::integral_constant<int, 4>{});
-        default: return cells(std::integral_constant<int, 8>{});
-        }
-    };
+    RangeTest rt;   // the gather wave's attribute test
     // keys of the candidates cid[0, c): one per lane, KEY_NONE past c
     auto score_cands = [&](uint32_t c) -> uint64_t {
         if (c == 0) return KEY_NONE;
@@ -1335,9 +1326,9 @@ __global__ void __launch_bounds__(128) pair_kernel(PhaseArgs a)
         typename Scorer::Ids ids0;
         sc.read_ids(cid, (int)c, 0, lane, ids0);
         int4 w0 = make_int4(0, 0, 0, 0), w1 = make_int4(0, 0, 0, 0);
-        if (lane < (int)c) load_attrs(my_id, w0, w1);
+        if (lane < (int)c) load_attr_record(ix, my_id, w0, w1);
         sc.score(ix.vectors, d, cid, (int)c, cd, lane, ids0);
-        const uint32_t phi = count_phi(w0, w1);
+        const uint32_t phi = rt.phi(w0, w1, ix.m_pad);
         wave_sync();
         return lane < (int)c ? make_key(phi, cd[lane], cid[lane]) : KEY_NONE;
     };
@@ -1375,32 +1366,7 @@ __global__ void __launch_bounds__(128) pair_kernel(PhaseArgs a)
         const uint32_t qi = bcast0(a.active[t]);
         if (!merger) {
             sc.load_query(a.queries, qi, d, lane);
-            phi0 = 0;
-#pragma unroll
-            for (int j = 0; j < BOA_MAX_M; ++j) {
-                int32_t l = 0;
-                uint32_t s = 0xFFFFFFFFu;
-                if (j < m) {
-                    int32_t lo = a.ranges[((size_t)qi * m + j) * 2 + 0];
-                    int32_t hi = a.ranges[((size_t)qi * m + j) * 2 + 1];
-                    bool none = false;
-                    if ((ix.f32_mask >> j) & 1u) {
-                        none = ((uint32_t)lo & 0x7FFFFFFFu) > 0x7F800000u ||
-                               ((uint32_t)hi & 0x7FFFFFFFu) > 0x7F800000u;
-                        lo = f32_ord((uint32_t)lo);
-                        hi = f32_ord((uint32_t)hi);
-                    }
-                    if (none || lo > hi) {
-                        phi0 += 1;
-                    } else {
-                        l = lo;
-                        s = (uint32_t)hi - (uint32_t)lo;
-                    }
-                }
-                asm volatile("" : "+v"(l), "+v"(s));
-                flo[j] = l;
-                fspan[j] = s;
-            }
+            rt.set(a.ranges, qi, m, ix.f32_mask);
         }
         // every phase restarts from the entry point (Alg. 1 calls Alg. 2 afresh)
         for (int p = a.p_begin; p < a.p_end; ++p) {
